@@ -1,0 +1,441 @@
+"""Pins of the CPU oracle against closed forms, invariants, brute force and
+independent library formulations (no GPU needed).
+
+Each test names what fixes the expected value: the paper's stated behaviour
+(confidence = softmax probability; unmask everything above the threshold, else
+the single most confident position; blockwise approximate caching with
+recompute after a block completes), a closed form, or a library routine.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+import synth
+
+rng = np.random.default_rng(1234)
+
+
+# ------------------------------------------------------------------ rounding
+def test_round_bf16_matches_torch_cast_on_fp32_values():
+    # torch's fp32 -> bf16 cast rounds to nearest even: a library pin.
+    x = rng.standard_normal(200_000).astype(np.float32) * np.float32(3.0)
+    # force exact ties and near-ties
+    bits = x.view(np.uint32)
+    bits[:1000] = (bits[:1000] & np.uint32(0xFFFF0000)) | np.uint32(0x8000)
+    bits[1000:2000] = (bits[1000:2000] & np.uint32(0xFFFF0000)) | np.uint32(0x7FFF)
+    bits[2000:3000] = (bits[2000:3000] & np.uint32(0xFFFF0000)) | np.uint32(0x8001)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(oracle.round_bf16(x), ref)
+
+
+def test_round_bf16_ties_to_even_closed_form():
+    one = 1.0
+    assert oracle.round_bf16(one + 2.0 ** -8) == 1.0            # tie -> even (1.0)
+    assert oracle.round_bf16(one + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6  # tie -> even (up)
+    assert oracle.round_bf16(one + 2.0 ** -8 + 2.0 ** -12) == 1.0 + 2.0 ** -7
+
+
+def test_synth_bf16_and_oracle_bf16_agree():
+    # the input generator's rounding and the oracle's own rounding are
+    # independent code; both must implement round-to-nearest-even.
+    x = rng.standard_normal(100_000).astype(np.float32)
+    a = synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(x)).astype(np.float64)
+    assert np.array_equal(a, oracle.round_bf16(x))
+
+
+# ----------------------------------------------------------------- generator
+def test_splitmix64_published_vector():
+    # SplitMix64 seeded with state 0 yields these first outputs (the
+    # reference outputs published with the generator).
+    from synth import _mix, GOLDEN
+    with np.errstate(over="ignore"):
+        s = np.arange(1, 4, dtype=np.uint64) * GOLDEN
+    out = _mix(s)
+    assert [int(v) for v in out] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4,
+                                     0x06C45D188009454F]
+
+
+def test_generator_moments_and_offsets():
+    x = synth.normal_f64(0, 77, 0, 400_000, 0.02)
+    assert abs(x.mean()) < 1e-4
+    assert abs(x.std() - 0.02) < 1e-4
+    # counter-based: any sub-range regenerates identically
+    y = synth.normal_f64(0, 77, 123_456, 1000, 0.02)
+    assert np.array_equal(x[123_456:124_456], y)
+    t = synth.tokens(5, 100_000, 2048)
+    assert t.min() >= 0 and t.max() <= 2047
+    assert abs(t.mean() - 1023.5) < 10
+
+
+# ------------------------------------------------------------------ rmsnorm
+def test_rmsnorm_matches_torch_rms_norm():
+    x = rng.standard_normal((7, 96))
+    g = rng.standard_normal(96)
+    ref = F.rms_norm(torch.from_numpy(x), (96,), torch.from_numpy(g), eps=1e-5).numpy()
+    assert np.allclose(oracle.rmsnorm(x, g, 1e-5), ref, rtol=1e-13, atol=1e-13)
+
+
+def test_rmsnorm_closed_form_and_scale_invariance():
+    c = 3.0
+    out = oracle.rmsnorm(np.full((1, 10), c), np.ones(10), 1e-5)
+    assert np.allclose(out, c / math.sqrt(c * c + 1e-5), rtol=1e-15)
+    x = rng.standard_normal((3, 64))
+    assert np.allclose(oracle.rmsnorm(5.0 * x, np.ones(64), 0.0),
+                       oracle.rmsnorm(x, np.ones(64), 0.0), rtol=1e-13)
+
+
+# --------------------------------------------------------------------- rope
+def test_rope_complex_rotation_form():
+    # rotate-half RoPE == multiplying (x_i + j x_{i+dh/2}) by exp(j pos w_i)
+    n, H, dh, theta = 5, 3, 16, 10000.0
+    x = rng.standard_normal((n, H, dh))
+    pos = np.array([0, 1, 7, 100, 4095])
+    half = dh // 2
+    w = theta ** (-np.arange(half) * 2.0 / dh)
+    zc = (x[..., :half] + 1j * x[..., half:]) * np.exp(1j * pos[:, None, None] * w[None, None, :])
+    ref = np.concatenate([zc.real, zc.imag], axis=-1)
+    assert np.allclose(oracle.rope(x, pos, theta), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_rope_identity_norm_and_relative_position():
+    dh = 32
+    x = rng.standard_normal((1, 1, dh))
+    assert np.array_equal(oracle.rope(x, np.array([0]), 1e4), x)
+    y = oracle.rope(np.repeat(x, 4, 0), np.array([3, 9, 50, 700]), 1e4)
+    assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x), rtol=1e-13)
+    q = rng.standard_normal((1, 1, dh))
+    k = rng.standard_normal((1, 1, dh))
+
+    def dot(m, n_):
+        return float(np.sum(oracle.rope(q, np.array([m]), 1e4) * oracle.rope(k, np.array([n_]), 1e4)))
+    assert math.isclose(dot(10, 3), dot(107, 100), rel_tol=1e-10)
+    assert not math.isclose(dot(10, 3), dot(10, 4), rel_tol=1e-6)
+
+
+# ---------------------------------------------------------------- attention
+def _sdpa_ref(q, k, v):
+    # torch library attention, non-causal, GQA via explicit head expansion
+    hq, hkv = q.shape[1], k.shape[1]
+    kk = torch.from_numpy(k).repeat_interleave(hq // hkv, dim=1)
+    vv = torch.from_numpy(v).repeat_interleave(hq // hkv, dim=1)
+    qq = torch.from_numpy(q)
+    out = F.scaled_dot_product_attention(qq.transpose(0, 1), kk.transpose(0, 1),
+                                         vv.transpose(0, 1), is_causal=False)
+    return out.transpose(0, 1).numpy()
+
+
+@pytest.mark.parametrize("hq,hkv", [(4, 4), (8, 2), (7, 1)])
+def test_attention_matches_torch_sdpa(hq, hkv):
+    q = rng.standard_normal((11, hq, 16))
+    k = rng.standard_normal((23, hkv, 16))
+    v = rng.standard_normal((23, hkv, 16))
+    assert np.allclose(oracle.attention(q, k, v), _sdpa_ref(q, k, v), rtol=1e-12, atol=1e-12)
+
+
+def test_attention_special_cases_and_permutations():
+    q = rng.standard_normal((6, 2, 8))
+    k1 = rng.standard_normal((1, 2, 8))
+    v1 = rng.standard_normal((1, 2, 8))
+    # a single key returns its value
+    assert np.allclose(oracle.attention(q, k1, v1), np.broadcast_to(v1, (6, 2, 8)))
+    # identical keys return the mean of the values
+    kk = np.repeat(k1, 5, 0)
+    vv = rng.standard_normal((5, 2, 8))
+    assert np.allclose(oracle.attention(q, kk, vv), np.broadcast_to(vv.mean(0), (6, 2, 8)))
+    # permuting queries permutes outputs; permuting keys with values changes nothing
+    k = rng.standard_normal((9, 2, 8))
+    v = rng.standard_normal((9, 2, 8))
+    o = oracle.attention(q, k, v)
+    pq = rng.permutation(6)
+    pk = rng.permutation(9)
+    assert np.allclose(oracle.attention(q[pq], k, v), o[pq], rtol=1e-13)
+    assert np.allclose(oracle.attention(q, k[pk], v[pk]), o, rtol=1e-13)
+
+
+# ------------------------------------------------------- softmax/confidence
+def test_softmax_sums_to_one_and_matches_torch():
+    z = rng.standard_normal((5, 1000)) * 4
+    p = oracle.softmax(z)
+    assert np.allclose(p.sum(-1), 1.0, atol=1e-12)
+    assert np.allclose(p, torch.softmax(torch.from_numpy(z), -1).numpy(), rtol=1e-12)
+    conf, tok = oracle.confidence(z)
+    assert np.allclose(conf, p.max(-1), rtol=1e-13)
+    assert np.array_equal(tok, p.argmax(-1))
+
+
+def test_confidence_closed_forms():
+    V = 126464
+    conf, tok = oracle.confidence(np.zeros((1, V)))
+    assert conf[0] == pytest.approx(1.0 / V, rel=1e-12) and tok[0] == 0
+    delta = 9.0
+    z = np.zeros((1, V))
+    z[0, 4321] = delta
+    conf, tok = oracle.confidence(z)
+    assert conf[0] == pytest.approx(math.exp(delta) / (math.exp(delta) + V - 1), rel=1e-12)
+    assert tok[0] == 4321
+    # equal maxima: lowest token id wins
+    z = np.zeros((1, 50))
+    z[0, [7, 3, 40]] = 2.0
+    assert oracle.confidence(z)[1][0] == 3
+
+
+# --------------------------------------------------------------- unmask rule
+def test_unmask_rule_threshold_extremes():
+    conf = np.array([0.2, 0.95, 0.5, 0.95, 0.91])
+    # threshold 1: exactly one, the most confident (lowest position on ties)
+    assert np.array_equal(np.nonzero(oracle.select_unmask(conf, 1.0))[0], [1])
+    # threshold 0: every masked position (confidence >= 1/V > 0)
+    assert oracle.select_unmask(conf, 0.0).all()
+    # strictly greater: a confidence equal to the threshold does not pass
+    assert np.array_equal(np.nonzero(oracle.select_unmask(conf, 0.91))[0], [1, 3])
+    # none above threshold -> forced single unmask
+    assert np.array_equal(np.nonzero(oracle.select_unmask(conf, 0.99))[0], [1])
+    assert oracle.select_unmask(np.zeros(0), 0.5).size == 0
+
+
+def test_unmask_rule_monotone_in_threshold():
+    for _ in range(50):
+        conf = rng.random(32)
+        gs = np.sort(rng.random(2))
+        a = oracle.select_unmask(conf, gs[0])
+        b = oracle.select_unmask(conf, gs[1])
+        assert np.all(a | ~b)   # U(g_small) contains U(g_large)
+
+
+# ------------------------------------------------------ tiny model fixtures
+TINY = synth.ModelConfig("t", 2, 32, 4, 2, 8, 48, 64, "f32")
+TINY_BF = synth.ModelConfig("tb", 2, 32, 4, 2, 8, 48, 64, "bf16")
+
+
+def _weights(cfg, n_layers=None, scale=1.0):
+    w = synth.model_weights(cfg, n_layers)
+    if scale != 1.0:
+        for lw in w["layers"]:
+            for k in ("wq", "wk", "wv", "wo", "wg", "wu", "wd"):
+                lw[k] = (lw[k] * scale).astype(np.float32)
+    return oracle.Weights.from_dict(w)
+
+
+def _torch_layer(cfg, lw, h, pos, kc, vc, r0, store):
+    """Independent formulation with torch library ops (linear, rms_norm, sdpa,
+    complex RoPE); returns new h and writes K/V rows."""
+    T = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    hq, hkv, dh, d = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d_model
+    h = T(h)
+    n = h.shape[0]
+    a = store(F.rms_norm(h, (d,), T(lw["attn_norm"]), eps=cfg.rms_eps))
+    q = F.linear(a, T(lw["wq"])).view(n, hq, dh)
+    k = F.linear(a, T(lw["wk"])).view(n, hkv, dh)
+    v = F.linear(a, T(lw["wv"])).view(n, hkv, dh)
+    half = dh // 2
+    w = cfg.rope_theta ** (-torch.arange(half, dtype=torch.float64) * 2.0 / dh)
+    rot = torch.polar(torch.ones(n, 1, half, dtype=torch.float64),
+                      torch.from_numpy(np.asarray(pos, np.float64))[:, None, None] * w)
+
+    def rp(x):
+        c = torch.complex(x[..., :half], x[..., half:]) * rot
+        return torch.cat([c.real, c.imag], -1)
+    q, k, v = store(rp(q)), store(rp(k)), store(v)
+    kc[r0:r0 + n] = k.numpy()
+    vc[r0:r0 + n] = v.numpy()
+    K = T(kc).repeat_interleave(hq // hkv, 1).transpose(0, 1)
+    Vv = T(vc).repeat_interleave(hq // hkv, 1).transpose(0, 1)
+    o = F.scaled_dot_product_attention(q.transpose(0, 1), K, Vv, is_causal=False)
+    o = store(o.transpose(0, 1).reshape(n, hq * dh))
+    h = h + F.linear(o, T(lw["wo"]))
+    a = store(F.rms_norm(h, (d,), T(lw["ffn_norm"]), eps=cfg.rms_eps))
+    act = store(F.silu(F.linear(a, T(lw["wg"]))) * F.linear(a, T(lw["wu"])))
+    return (h + F.linear(act, T(lw["wd"]))).numpy()
+
+
+@pytest.mark.parametrize("cfg", [TINY, TINY_BF], ids=["f32", "bf16"])
+def test_layer_forward_matches_torch_formulation(cfg):
+    W = _weights(cfg, scale=10.0)   # larger weights: non-trivial attention
+    L = 20
+    h0 = rng.standard_normal((L, cfg.d_model))
+    if cfg.dtype == "bf16":
+        store = lambda t: t.to(torch.bfloat16).to(torch.float64)
+    else:
+        store = lambda t: t
+    for r0, r1 in [(0, L), (6, 13)]:
+        kc_a = rng.standard_normal((L, cfg.n_kv_heads, cfg.head_dim))
+        vc_a = rng.standard_normal((L, cfg.n_kv_heads, cfg.head_dim))
+        kc_b, vc_b = kc_a.copy(), vc_a.copy()
+        h = h0[r0:r1]
+        out = oracle.layer_forward(cfg, W.layer(0), h, r0, r1, kc_a, vc_a)
+        ref = _torch_layer(cfg, W.layer(0), h, np.arange(r0, r1), kc_b, vc_b, r0, store)
+        tol = 1e-10 if cfg.dtype == "f32" else 1e-6
+        assert np.allclose(out, ref, rtol=tol, atol=tol)
+        assert np.allclose(kc_a, kc_b, atol=tol) and np.allclose(vc_a, vc_b, atol=tol)
+
+
+def test_zero_gate_leaves_only_attention_update():
+    cfg = TINY
+    W = _weights(cfg)
+    L = 12
+    h = rng.standard_normal((L, cfg.d_model))
+    lw_g = dict(W.layer(0), wg=np.zeros_like(W.layer(0)["wg"]))
+    lw_d = dict(W.layer(0), wd=np.zeros_like(W.layer(0)["wd"]))
+    kc = np.zeros((L, cfg.n_kv_heads, cfg.head_dim))
+    vc = np.zeros_like(kc)
+    a = oracle.layer_forward(cfg, lw_g, h, 0, L, kc, vc)
+    b = oracle.layer_forward(cfg, lw_d, h, 0, L, kc.copy(), vc.copy())
+    assert np.array_equal(a, b)
+
+
+def test_head_logits_matches_torch():
+    cfg = TINY_BF
+    W = _weights(cfg)
+    h = rng.standard_normal((5, cfg.d_model)) * 3
+    z = oracle.head_logits(cfg, W, h, 7.5)
+    T = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    u = F.rms_norm(T(h), (cfg.d_model,), T(W.globals["final_norm"]), eps=cfg.rms_eps)
+    u = u.to(torch.bfloat16).to(torch.float64)
+    ref = F.linear(u, T(W.globals["lm_head"])).numpy() * 7.5
+    assert np.allclose(z, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_masked_positions_embed_mask_token():
+    cfg = TINY
+    W = _weights(cfg)
+    req = oracle.Request.new(np.array([3, 5, 7]), 4, 2, 0.9, cfg.mask_id)
+    req.tokens[4] = 11       # a stale token under a mask must not matter
+    x = oracle.embed_rows(cfg, W, req, 0, 7)
+    assert np.array_equal(x[0], W.globals["embed"][3])
+    assert np.array_equal(x[4], W.globals["embed"][cfg.mask_id])
+
+
+# ------------------------------------------------------------ step semantics
+def _prompt(cfg, n, seed=7):
+    return synth.tokens(seed, n, cfg.vocab)
+
+
+def _fresh(cfg, P, G, B, gamma, seed=7):
+    return oracle.Request.new(_prompt(cfg, P, seed), G, B, gamma, cfg.mask_id)
+
+
+@pytest.mark.parametrize("mode", ["dual", "prefix"])
+def test_cache_without_approximation_equals_recompute(mode):
+    """Refresh on a state, then a cached step on the same state: equal to the
+    no-cache step on that state (nothing is stale)."""
+    cfg = TINY
+    W = _weights(cfg, scale=8.0)
+    inv_tau = 30.0
+    base = _fresh(cfg, 9, 12, 4, 0.9)
+    # unmask a few positions of block 1 so the state is generic
+    base.tokens[9:13] = [1, 2, 3, 4]
+    base.mask[9:13] = False
+    base.k = 1
+    base.tokens[14] = 5
+    base.mask[14] = False
+    import copy
+    r_none = copy.deepcopy(base)
+    h_n, rows_n, _ = oracle.step_forward(cfg, W, r_none, "none")
+    res_n = oracle.finish_step(cfg, W, r_none, h_n, rows_n, True, inv_tau, keep_logits=True)
+
+    r_c = copy.deepcopy(base)
+    oracle.step_forward(cfg, W, r_c, mode, refresh=True)     # refresh, no unmask
+    h_c, rows_c, refresh = oracle.step_forward(cfg, W, r_c, mode)
+    assert not refresh and rows_c[0] == 13
+    res_c = oracle.finish_step(cfg, W, r_c, h_c, rows_c, refresh, inv_tau, keep_logits=True)
+    assert np.allclose(res_c.logits, res_n.logits, rtol=1e-11, atol=1e-11)
+    assert np.array_equal(res_c.positions, res_n.positions)
+    assert np.array_equal(res_c.tokens, res_n.tokens)
+
+
+def test_stale_cache_is_an_approximation():
+    cfg = TINY
+    W = _weights(cfg, scale=8.0)
+    import copy
+    req = _fresh(cfg, 9, 8, 4, 0.0)
+    oracle.step_forward(cfg, W, req, "dual", refresh=True)
+    req.tokens[9:11] = [3, 4]
+    req.mask[9:11] = False       # state changes after the refresh
+    r2 = copy.deepcopy(req)
+    h_c, rows_c, _ = oracle.step_forward(cfg, W, req, "dual")
+    res_c = oracle.finish_step(cfg, W, req, h_c, rows_c, False, 20.0, keep_logits=True)
+    h_n, rows_n, _ = oracle.step_forward(cfg, W, r2, "none")
+    res_n = oracle.finish_step(cfg, W, r2, h_n, rows_n, True, 20.0, keep_logits=True)
+    assert not np.allclose(res_c.logits, res_n.logits, rtol=1e-6)
+
+
+@pytest.mark.parametrize("mode", ["none", "dual", "prefix"])
+def test_threshold_one_unmasks_one_per_step(mode):
+    cfg = TINY
+    W = _weights(cfg, scale=6.0)
+    P, G, B = 6, 8, 4
+    reqs, trace = oracle.generate(cfg, W, [_prompt(cfg, P)], [G], [1.0], B, mode, 25.0)
+    assert len(trace) == G
+    assert all(len(st[0][1].positions) == 1 for st in trace)
+    # the unmasked position is the most confident masked one
+    for st in trace:
+        r = st[0][1]
+        assert r.positions[0] == r.masked_positions[np.argmax(r.masked_conf)]
+    if mode != "none":
+        # each block: one recompute step, then block-1 cache steps
+        assert [st[0][1].refresh for st in trace] == ([True] + [False] * (B - 1)) * (G // B)
+    assert not reqs[0].mask.any()
+
+
+def test_threshold_zero_unmasks_blocks_and_modes_agree():
+    cfg = TINY
+    W = _weights(cfg, scale=6.0)
+    P, G, B = 5, 12, 4
+    outs = {}
+    for mode in ("none", "dual", "prefix"):
+        reqs, trace = oracle.generate(cfg, W, [_prompt(cfg, P)], [G], [0.0], B, mode, 25.0)
+        assert len(trace) == G // B
+        assert all(st[0][1].refresh for st in trace)
+        assert all(len(st[0][1].positions) == B for st in trace)
+        outs[mode] = reqs[0].tokens.copy()
+    assert np.array_equal(outs["none"], outs["dual"])
+    assert np.array_equal(outs["none"], outs["prefix"])
+
+
+def test_ragged_last_block():
+    cfg = TINY
+    W = _weights(cfg, scale=6.0)
+    reqs, trace = oracle.generate(cfg, W, [_prompt(cfg, 3)], [10], [1.0], 4, "dual", 25.0)
+    assert len(trace) == 10
+    assert [st[0][1].refresh for st in trace] == [True, False, False, False] * 2 + [True, False]
+
+
+def test_batch_requests_are_independent():
+    cfg = TINY
+    W = _weights(cfg, scale=6.0)
+    p0, p1 = _prompt(cfg, 5, 1), _prompt(cfg, 9, 2)
+    both, _ = oracle.generate(cfg, W, [p0, p1], [8, 4], [0.5, 0.9], 4, "dual", 25.0)
+    a, _ = oracle.generate(cfg, W, [p0], [8], [0.5], 4, "dual", 25.0)
+    b, _ = oracle.generate(cfg, W, [p1], [4], [0.9], 4, "dual", 25.0)
+    assert np.array_equal(both[0].tokens, a[0].tokens)
+    assert np.array_equal(both[1].tokens, b[0].tokens)
+
+
+def test_prompt_positions_never_change():
+    cfg = TINY
+    W = _weights(cfg, scale=6.0)
+    p = _prompt(cfg, 7)
+    reqs, _ = oracle.generate(cfg, W, [p], [8], [0.7], 4, "prefix", 25.0)
+    assert np.array_equal(reqs[0].tokens[:7], p)
+
+
+# --------------------------------------------------------------- calibration
+def test_top_prob_monotone_and_tau_star():
+    z = rng.standard_normal(500) * 2
+    taus = np.geomspace(1e-3, 1e2, 40)
+    f = [oracle.top_prob(z, t) for t in taus]
+    assert all(a >= b - 1e-15 for a, b in zip(f, f[1:]))
+    ts = oracle.tau_star(z, 0.9)
+    assert oracle.top_prob(z, ts) > 0.9
+    assert oracle.top_prob(z, ts * (1 + 1e-9)) <= 0.9 + 1e-6
+
+
+def test_calibration_hits_share():
+    zs = rng.standard_normal((40, 300)) * 2
+    tau, inv_tau, achieved, k, n = oracle.calibrate(zs, 0.9, 0.3)
+    assert k == 12 and n == 40
+    assert achieved == pytest.approx(12 / 40)
