@@ -1,0 +1,195 @@
+/*
+ * dlm.h - C ABI of the MI355X (gfx950) denoising-step library, libdlm.so.
+ *
+ * One call of dlm_denoise_step is one batched denoising step of a
+ * masked-diffusion transformer (paper: "Background and Challenges",
+ * Diffusion Language Models): the prompt plus [MASK] tokens pass through a
+ * bidirectional-attention Transformer, every masked position of the active
+ * block gets a prediction and a confidence (its softmax probability), the
+ * positions whose confidence exceeds the request's threshold are unmasked,
+ * and when none does the most confident one is unmasked alone. With
+ * approximate KV caching ("Support for Approximate Caching"; "Supporting
+ * Approximate KV Caching") a step is either a recompute step, which processes
+ * every token and rewrites the request's cache, or a cache step, which
+ * recomputes only the active block (dual cache) or the active block and the
+ * positions after it (prefix cache) and reads every other key/value from the
+ * cache written by the last recompute step.
+ *
+ * Conventions shared by every entry point:
+ *  - All device memory is owned by the caller. The library never allocates or
+ *    frees device memory and never synchronises a stream; work is enqueued on
+ *    the stream passed in (a hipStream_t given as void*; NULL is the default
+ *    stream) and results are valid once the caller has synchronised it.
+ *  - dlm_model and dlm_cache are opaque host handles that borrow the caller's
+ *    device pointers; those must outlive the handles. *_destroy frees host
+ *    state only.
+ *  - Every argument is validated on the host before anything is enqueued. On
+ *    any non-OK status nothing is enqueued and no handle changes state; the
+ *    reason is in dlm_last_error() (thread-local, valid until the next call on
+ *    the same thread).
+ *  - Handles are thread-compatible, not thread-safe: calls that share a handle
+ *    must be serialised by the caller.
+ *
+ * Data types: DLM_BF16 models store weights, normed activations, Q/K/V and the
+ * KV cache in bf16 and accumulate in fp32; the residual stream is fp32.
+ * DLM_F32 models store everything in fp32. Norm gains are always fp32.
+ * Matrices are row-major [out, in] (in contiguous).
+ */
+#ifndef DLM_H
+#define DLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DLM_OK = 0,
+  DLM_EINVAL = -1,        /* malformed argument (null pointer, bad shape, bad threshold) */
+  DLM_ESIZE = -2,         /* a buffer is too small (workspace, cache buffer, limits)     */
+  DLM_EHIP = -3,          /* a HIP runtime call failed; its message is in last_error    */
+  DLM_ESTATE = -4,        /* cache step on a slot whose cache is not current             */
+  DLM_EUNSUPPORTED = -5   /* configuration outside what the kernels implement           */
+} dlm_status;
+
+typedef enum { DLM_F32 = 0, DLM_BF16 = 1 } dlm_dtype;
+
+typedef enum {
+  DLM_CACHE_NONE = 0,     /* every step recomputes the whole sequence (exact)          */
+  DLM_CACHE_PREFIX = 1,   /* cache steps recompute [block_start, seq_len)               */
+  DLM_CACHE_DUAL = 2      /* cache steps recompute [block_start, block_start+block_len) */
+} dlm_cache_mode;
+
+enum {
+  DLM_MAX_BLOCK = 64,     /* largest block length (one 64-lane wavefront per request) */
+  DLM_MAX_REQ = 64,       /* largest number of requests in one step                     */
+  DLM_MAX_SEQ = 8192      /* largest sequence length                                    */
+};
+
+/* Request flag: this step is a recompute step (whole sequence, cache rewritten). */
+#define DLM_REQ_REFRESH 1
+
+/* Model shape. Supported: head_dim 64 or 128, d_model and d_ffn multiples of 64,
+ * n_q_heads a multiple of n_kv_heads, mask_id in [0, vocab). inv_tau scales the
+ * logits before the softmax (1/temperature). */
+typedef struct dlm_config {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab, mask_id;
+  float rms_eps, rope_theta, inv_tau;
+  int32_t dtype;          /* dlm_dtype */
+} dlm_config;
+
+/* Per-layer weights (device pointers). */
+typedef struct dlm_layer_weights {
+  const float* attn_norm; /* [d_model] fp32                                               */
+  const void* w_qkv;      /* [(n_q_heads + 2 n_kv_heads) head_dim, d_model]: Q rows, then K, then V */
+  const void* w_o;        /* [d_model, n_q_heads head_dim]                                 */
+  const float* ffn_norm;  /* [d_model] fp32                                               */
+  const void* w_gate_up;  /* [2 d_ffn, d_model]: gate rows, then up rows                   */
+  const void* w_down;     /* [d_model, d_ffn]                                              */
+} dlm_layer_weights;
+
+typedef struct dlm_weights {
+  const void* embed;      /* [vocab, d_model]                                              */
+  const void* lm_head;    /* [vocab, d_model] (untied)                                     */
+  const float* final_norm;/* [d_model] fp32                                               */
+  const dlm_layer_weights* layers; /* host array of n_layers entries, copied by load     */
+} dlm_weights;
+
+/* One request of a batched step (host struct). Positions are 0-based within the
+ * request; position j of request r lives at tokens[tok_offset + j]. */
+typedef struct dlm_req {
+  int32_t slot;           /* cache slot, unique within a batch                          */
+  int32_t seq_len;        /* prompt + generation length                                  */
+  int32_t prompt_len;     /* positions [0, prompt_len) are the prompt                    */
+  int32_t block_start;    /* first position of the active block (>= prompt_len)          */
+  int32_t block_len;      /* 1..DLM_MAX_BLOCK, block_start + block_len <= seq_len         */
+  int32_t tok_offset;     /* offset of position 0 in the packed tokens/mask arrays       */
+  int32_t flags;          /* DLM_REQ_REFRESH or 0                                        */
+} dlm_req;
+
+typedef struct dlm_batch {
+  int32_t n_req;          /* 1..DLM_MAX_REQ                                              */
+  const dlm_req* reqs;    /* host array [n_req]                                          */
+  int32_t* tokens;        /* device, packed token ids; updated in place                  */
+  uint8_t* mask;          /* device, packed, 1 = [MASK]; updated in place                */
+  int32_t mode;           /* dlm_cache_mode                                              */
+} dlm_batch;
+
+/* Step outputs (device). Request r's entries start at r * DLM_MAX_BLOCK. */
+typedef struct dlm_step_out {
+  int32_t* n_unmasked;    /* [n_req] number of positions unmasked this step              */
+  int32_t* pos;           /* [n_req * DLM_MAX_BLOCK] unmasked positions, ascending        */
+  int32_t* tok;           /* [n_req * DLM_MAX_BLOCK] their new tokens                     */
+  float* conf;            /* [n_req * DLM_MAX_BLOCK] their confidences                    */
+  float* block_conf;      /* optional [n_req * DLM_MAX_BLOCK]: confidence of every block
+                             position masked at step start (index = pos - block_start),
+                             -1 for positions that were already unmasked                  */
+  int32_t* block_tok;     /* optional, same layout: prediction of each masked position   */
+} dlm_step_out;
+
+typedef struct dlm_model dlm_model;
+typedef struct dlm_cache dlm_cache;
+
+/* Validate the configuration and record the caller's weight pointers. */
+dlm_status dlm_load_weights(const dlm_config* cfg, const dlm_weights* w, dlm_model** out);
+void dlm_model_destroy(dlm_model* m);
+
+/* Workspace bytes for steps of at most max_rows recomputed rows (sum over
+ * requests of the rows each step recomputes) and max_reqs requests. */
+dlm_status dlm_workspace_bytes(const dlm_model* m, int32_t max_rows, int32_t max_reqs,
+                               size_t* out_bytes);
+
+/* Carve n_slots fixed KV slots of max_seq_len positions out of the caller's
+ * buffer (post-RoPE keys and values of every layer; the output length of a
+ * request is known in advance, so slots are fixed-size). With dev_buf == NULL
+ * only *required_bytes is written. Every slot starts invalid: its first step
+ * must be a recompute step. */
+dlm_status dlm_kv_cache_alloc(const dlm_model* m, int32_t n_slots, int32_t max_seq_len,
+                              void* dev_buf, size_t buf_bytes, size_t* required_bytes,
+                              dlm_cache** out);
+void dlm_cache_destroy(dlm_cache* c);
+/* Mark a slot stale (its next step must be a recompute step). */
+dlm_status dlm_cache_invalidate(dlm_cache* c, int32_t slot);
+
+/* One batched denoising step. thresholds: host [n_req], each in [0, 1].
+ * Requests flagged DLM_REQ_REFRESH (all requests when mode is DLM_CACHE_NONE)
+ * recompute every position and rewrite their slot; the others recompute the
+ * rows their mode names and need a slot refreshed at the same block_start
+ * (else DLM_ESTATE). Masked positions of the active block get a prediction;
+ * those with confidence > threshold are unmasked (tokens[] and mask[] updated
+ * in place); if none passes, the most confident one (lowest position on ties)
+ * is unmasked. */
+dlm_status dlm_denoise_step(dlm_model* m, dlm_cache* c, const dlm_batch* b,
+                            const float* thresholds, const dlm_step_out* out,
+                            void* workspace, size_t ws_bytes, void* stream);
+
+/* Recompute every position of every request of the batch and rewrite their
+ * slots without unmasking anything (prefill, resume, or rebuilding a slot). */
+dlm_status dlm_cache_refresh(dlm_model* m, dlm_cache* c, const dlm_batch* b,
+                             void* workspace, size_t ws_bytes, void* stream);
+
+/* Test hook: run the forward of a step (same rows and cache writes as
+ * dlm_denoise_step, nothing unmasked) and write the scaled logits z = logits *
+ * inv_tau of every active-block position: rows in request order, positions
+ * ascending, logits_out [sum block_len, vocab] fp32 (device). */
+dlm_status dlm_debug_logits(dlm_model* m, dlm_cache* c, const dlm_batch* b,
+                            float* logits_out, void* workspace, size_t ws_bytes,
+                            void* stream);
+
+/* The fused LM head alone: for each of m_rows final-normed hidden rows
+ * (device, [m_rows, d_model] in the model dtype), conf[i] = max softmax(z_i) and
+ * tok[i] = lowest argmax z_i, z_i = (u_i W_lm^T) * inv_tau. The logits are not
+ * stored. Needs dlm_workspace_bytes(m, m_rows, 1) of workspace. */
+dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
+                               float* conf, int32_t* tok, void* workspace,
+                               size_t ws_bytes, void* stream);
+
+/* Message for the last non-OK status on this thread ("" if none). */
+const char* dlm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DLM_H */

@@ -1,0 +1,98 @@
+// Launch functions of the denoising-step kernels (internal to libdlm.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dlm {
+
+constexpr int kMaxReq = 64;
+constexpr int kMaxBlock = 64;
+constexpr int kQTile = 64;      // query rows per attention block / rows per RoPE tile
+
+// Per-request plan of one step, passed by value as a kernel argument.
+struct ReqPlan {
+  int row0;      // first packed recompute row
+  int nrows;     // recompute rows
+  int pos0;      // position of the first recompute row
+  int seq_len;   // keys attended (all positions of the slot)
+  int slot;
+  int tok_off;   // offset of position 0 in tokens/mask
+  int blk_s;     // active block [blk_s, blk_s + blk_len)
+  int blk_len;
+  int tile0;     // first 64-row tile of this request (attention / RoPE grids)
+  int blk0;      // offset of this request's block rows in the packed block-row order
+  float gamma;   // threshold
+};
+struct StepPlan {
+  int n_req;
+  int n_rows;    // total recompute rows N
+  int n_tiles;   // total 64-row tiles
+  int n_blk;     // total block rows
+  ReqPlan r[kMaxReq];
+};
+
+// Row -> request lookup (requests are few; plan rows are ascending).
+__device__ __forceinline__ int plan_req_of_row(const StepPlan& p, int row) {
+  int r = 0;
+  while (r + 1 < p.n_req && p.r[r + 1].row0 <= row) ++r;
+  return r;
+}
+__device__ __forceinline__ int plan_req_of_tile(const StepPlan& p, int tile) {
+  int r = 0;
+  while (r + 1 < p.n_req && p.r[r + 1].tile0 <= tile) ++r;
+  return r;
+}
+
+// ---- GEMM family (gemm.hip) ----
+int gemm_split_count(int M, int N, int K, int num_cu);
+template <typename T>
+hipError_t gemm_store_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
+                          int splits, float* C, int ldc, hipStream_t st);
+template <typename T>
+hipError_t gemm_add_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
+                        float* C, int ldc, hipStream_t st);
+template <typename T>
+hipError_t gemm_scaled_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
+                           float scale, float* C, int ldc, hipStream_t st);
+template <typename T>
+hipError_t gemm_swiglu(const T* A, int lda, const T* W, int ldw, int M, int F, int K,
+                       T* out, int ldo, hipStream_t st);
+int lm_head_tiles(int V);
+template <typename T>
+hipError_t gemm_lm_head(const T* U, int ldu, const T* W, int M, int V, int K, float inv_tau,
+                        float* pm, float* ps, int* pi, int ld, hipStream_t st);
+
+// ---- per-row kernels (rowwise.hip) ----
+template <typename T>
+hipError_t embed_rows(const StepPlan& p, const T* E, int d, int vocab, int mask_id,
+                      const int32_t* tokens, const uint8_t* mask, float* h, hipStream_t st);
+template <typename T>
+hipError_t rmsnorm_rows(const float* h, const float* g, int n, int d, float eps, T* out,
+                        hipStream_t st);
+hipError_t rope_table(const StepPlan& p, int head_dim, float theta, float2* cs, hipStream_t st);
+template <typename T>
+hipError_t qkv_rope_scatter(const StepPlan& p, const float* qkv, int splits, long split_stride,
+                            const float2* cs, int hq, int hkv, int dh, T* q_out,
+                            T* kcache, T* vcache, int s_max, hipStream_t st);
+hipError_t add_partials(const float* part, int splits, long split_stride, int n, int d, float* h,
+                        hipStream_t st);
+hipError_t lm_select_rows(const StepPlan& p, const uint8_t* mask, int all_rows, int* lm_rows,
+                          int* lm_count, int* req_lm_off, int* req_lm_cnt, hipStream_t st);
+template <typename T>
+hipError_t final_norm_gather(const float* h, const float* g, const int* lm_rows,
+                             const int* lm_count, int m_max, int d, float eps, T* u,
+                             hipStream_t st);
+hipError_t lm_combine(const float* pm, const float* ps, const int* pi, int tiles, int ld,
+                      const int* lm_count, int m_max, float* conf, int* tok, hipStream_t st);
+hipError_t unmask_select(const StepPlan& p, const float* conf, const int* tok,
+                         const int* req_lm_off, int32_t* tokens, uint8_t* mask,
+                         int32_t* n_unmasked, int32_t* out_pos, int32_t* out_tok,
+                         float* out_conf, float* blk_conf, int32_t* blk_tok, hipStream_t st);
+
+// ---- attention (attention.hip) ----
+template <typename T>
+hipError_t attention(const StepPlan& p, const T* q, const T* kcache, const T* vcache,
+                     int s_max, int hq, int hkv, int dh, T* out, hipStream_t st);
+
+}  // namespace dlm

@@ -1,0 +1,406 @@
+// Row-wise kernels of the denoising step: embedding gather, RMSNorm, RoPE and
+// the key/value cache writes, split-K reduction into the residual stream, the
+// selection of the rows that need a prediction, the final norm, the combine of
+// the per-vocab-tile softmax statistics and the threshold/compaction step.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace dlm {
+
+// ------------------------------------------------------------ embedding --
+// h[n] = E[mask ? mask_id : token] for every recompute row n (fp32 residual).
+// Token ids outside [0, vocab) are read as [MASK].
+template <typename T>
+__global__ void embed_kernel(StepPlan p, const T* __restrict__ E, int d, int vocab, int mask_id,
+                             const int32_t* __restrict__ tokens, const uint8_t* __restrict__ mask,
+                             float* __restrict__ h) {
+  const int n = blockIdx.x;
+  const int r = plan_req_of_row(p, n);
+  const ReqPlan& q = p.r[r];
+  const int pos = q.pos0 + (n - q.row0);
+  const long ti = (long)q.tok_off + pos;
+  const int tk = tokens[ti];
+  const int id = (mask[ti] || tk < 0 || tk >= vocab) ? mask_id : tk;
+  const T* src = E + (long)id * d;
+  float* dst = h + (long)n * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) dst[j] = to_f32(src[j]);
+}
+
+template <typename T>
+hipError_t embed_rows(const StepPlan& p, const T* E, int d, int vocab, int mask_id,
+                      const int32_t* tokens, const uint8_t* mask, float* h, hipStream_t st) {
+  if (p.n_rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_kernel<T>, dim3(p.n_rows), dim3(256), 0, st, p, E, d, vocab, mask_id,
+                     tokens, mask, h);
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------------- rmsnorm --
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = red[0] + red[1] + red[2] + red[3];
+  __syncthreads();
+  return t;
+}
+
+// out[n] = h[n] / sqrt(mean(h[n]^2) + eps) * g, fp32 math, stored as T.
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h,
+                                                      const float* __restrict__ g, int d,
+                                                      float eps, T* __restrict__ out,
+                                                      const int* __restrict__ rows,
+                                                      const int* __restrict__ count) {
+  __shared__ float red[4];
+  const int i = blockIdx.x;
+  if (count && i >= *count) return;
+  const int src_row = rows ? rows[i] : i;
+  const float* x = h + (long)src_row * d;
+  float ss = 0.f;
+  for (int j = threadIdx.x * 4; j < d; j += 1024) {
+    float4 v = *reinterpret_cast<const float4*>(x + j);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  const float inv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)d + eps);
+  T* o = out + (long)i * d;
+  for (int j = threadIdx.x * 4; j < d; j += 1024) {
+    float4 v = *reinterpret_cast<const float4*>(x + j);
+    float4 gg = *reinterpret_cast<const float4*>(g + j);
+    o[j + 0] = from_f32<T>(v.x * inv * gg.x);
+    o[j + 1] = from_f32<T>(v.y * inv * gg.y);
+    o[j + 2] = from_f32<T>(v.z * inv * gg.z);
+    o[j + 3] = from_f32<T>(v.w * inv * gg.w);
+  }
+}
+
+template <typename T>
+hipError_t rmsnorm_rows(const float* h, const float* g, int n, int d, float eps, T* out,
+                        hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, h, g, d, eps, out,
+                     (const int*)nullptr, (const int*)nullptr);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t final_norm_gather(const float* h, const float* g, const int* lm_rows,
+                             const int* lm_count, int m_max, int d, float eps, T* u,
+                             hipStream_t st) {
+  if (m_max == 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(m_max), dim3(256), 0, st, h, g, d, eps, u, lm_rows,
+                     lm_count);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------- RoPE --
+// cs[n][i] = (cos, sin) of pos(n) * theta^(-2i/dh), angle and trig in fp64.
+__global__ void rope_table_kernel(StepPlan p, int half, double log_theta, float2* cs) {
+  const int n = blockIdx.x;
+  const int r = plan_req_of_row(p, n);
+  const double pos = (double)(p.r[r].pos0 + (n - p.r[r].row0));
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    const double freq = exp(-log_theta * (double)(2 * i) / (double)(2 * half));
+    double s, c;
+    sincos(pos * freq, &s, &c);
+    cs[(long)n * half + i] = make_float2((float)c, (float)s);
+  }
+}
+
+hipError_t rope_table(const StepPlan& p, int head_dim, float theta, float2* cs, hipStream_t st) {
+  if (p.n_rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(p.n_rows), dim3(64), 0, st, p, head_dim / 2,
+                     log((double)theta), cs);
+  return hipGetLastError();
+}
+
+// One block = one 64-row tile of one request x one head slot:
+//   y <  hq         : query head y   -> rotated, stored to q_out[n][y*dh..]
+//   y >= hq         : kv head y - hq -> rotated key to K[slot][j][pos][:],
+//                                       value (transposed in LDS) to V[slot][j][:][pos]
+// The fp32 input is the sum of the split-K partial slices of the QKV GEMM.
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void qkv_rope_scatter_kernel(
+    StepPlan p, const float* __restrict__ qkv, int splits, long split_stride,
+    const float2* __restrict__ cs, int hq, int hkv, T* __restrict__ q_out,
+    T* __restrict__ kcache, T* __restrict__ vcache, int s_max) {
+  constexpr int HALF = DH / 2;
+  __shared__ T vt[DH][kQTile + 2];
+  const int tile = blockIdx.x;
+  const int y = blockIdx.y;
+  const int r = plan_req_of_tile(p, tile);
+  const ReqPlan& q = p.r[r];
+  const int lrow0 = (tile - q.tile0) * kQTile;           // first row within request
+  const int nvalid = min(kQTile, q.nrows - lrow0);
+  const int qkv_dim = (hq + 2 * hkv) * DH;
+  const int row_base = q.row0 + lrow0;
+  const int pos_base = q.pos0 + lrow0;
+
+  auto load = [&](int n, int col) {
+    const float* src = qkv + (long)n * qkv_dim + col;
+    float v = src[0];
+    for (int s = 1; s < splits; ++s) v += src[(long)s * split_stride];
+    return v;
+  };
+
+  if (y < hq) {
+    for (int idx = threadIdx.x; idx < nvalid * HALF; idx += blockDim.x) {
+      const int rr = idx / HALF, i = idx % HALF;
+      const int n = row_base + rr;
+      const float x1 = load(n, y * DH + i), x2 = load(n, y * DH + i + HALF);
+      const float2 c = cs[(long)n * HALF + i];
+      T* o = q_out + (long)n * hq * DH + y * DH;
+      o[i] = from_f32<T>(x1 * c.x - x2 * c.y);
+      o[i + HALF] = from_f32<T>(x2 * c.x + x1 * c.y);
+    }
+    return;
+  }
+  const int j = y - hq;
+  T* kb = kcache + ((long)(q.slot * hkv + j) * s_max) * DH;
+  T* vb = vcache + ((long)(q.slot * hkv + j) * DH) * s_max;
+  const int kcol = hq * DH + j * DH;
+  const int vcol = (hq + hkv) * DH + j * DH;
+  for (int idx = threadIdx.x; idx < nvalid * HALF; idx += blockDim.x) {
+    const int rr = idx / HALF, i = idx % HALF;
+    const int n = row_base + rr;
+    const float x1 = load(n, kcol + i), x2 = load(n, kcol + i + HALF);
+    const float2 c = cs[(long)n * HALF + i];
+    T* o = kb + (long)(pos_base + rr) * DH;
+    o[i] = from_f32<T>(x1 * c.x - x2 * c.y);
+    o[i + HALF] = from_f32<T>(x2 * c.x + x1 * c.y);
+  }
+  for (int idx = threadIdx.x; idx < nvalid * DH; idx += blockDim.x) {
+    const int rr = idx / DH, d = idx % DH;
+    vt[d][rr] = from_f32<T>(load(row_base + rr, vcol + d));
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < nvalid * DH; idx += blockDim.x) {
+    const int d = idx / nvalid, rr = idx % nvalid;
+    vb[(long)d * s_max + pos_base + rr] = vt[d][rr];
+  }
+}
+
+template <typename T>
+hipError_t qkv_rope_scatter(const StepPlan& p, const float* qkv, int splits, long split_stride,
+                            const float2* cs, int hq, int hkv, int dh, T* q_out,
+                            T* kcache, T* vcache, int s_max, hipStream_t st) {
+  if (p.n_tiles == 0) return hipSuccess;
+  dim3 g(p.n_tiles, hq + hkv);
+  if (dh == 128)
+    hipLaunchKernelGGL((qkv_rope_scatter_kernel<T, 128>), g, dim3(256), 0, st, p, qkv, splits,
+                       split_stride, cs, hq, hkv, q_out, kcache, vcache, s_max);
+  else if (dh == 64)
+    hipLaunchKernelGGL((qkv_rope_scatter_kernel<T, 64>), g, dim3(256), 0, st, p, qkv, splits,
+                       split_stride, cs, hq, hkv, q_out, kcache, vcache, s_max);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------ split-K reduction --
+// h[n][j] += sum_s part[s][n][j], slices summed in order s = 0, 1, ...
+__global__ void add_partials_kernel(const float* __restrict__ part, int splits, long stride,
+                                    long total4, float* __restrict__ h) {
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < total4;
+       i += (long)gridDim.x * blockDim.x) {
+    float4 acc = reinterpret_cast<const float4*>(part)[i];
+    for (int s = 1; s < splits; ++s) {
+      float4 v = reinterpret_cast<const float4*>(part + s * stride)[i];
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    float4 o = reinterpret_cast<float4*>(h)[i];
+    o.x += acc.x; o.y += acc.y; o.z += acc.z; o.w += acc.w;
+    reinterpret_cast<float4*>(h)[i] = o;
+  }
+}
+
+hipError_t add_partials(const float* part, int splits, long split_stride, int n, int d, float* h,
+                        hipStream_t st) {
+  long total4 = (long)n * d / 4;
+  if (total4 == 0) return hipSuccess;
+  int blocks = (int)std::min<long>((total4 + 255) / 256, 4096);
+  hipLaunchKernelGGL(add_partials_kernel, dim3(blocks), dim3(256), 0, st, part, splits,
+                     split_stride, total4, h);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------- LM row selection --
+// Rows that get a prediction: the masked positions of each active block
+// (all block positions when all_rows != 0), in request order, ascending
+// position. One wave per request counts with a ballot; a single block then
+// scans the counts in request order. Output indices are packed recompute rows.
+__global__ __launch_bounds__(1024) void lm_select_kernel(StepPlan p, const uint8_t* __restrict__ mask,
+                                                         int all_rows, int* __restrict__ lm_rows,
+                                                         int* __restrict__ lm_count,
+                                                         int* __restrict__ req_off,
+                                                         int* __restrict__ req_cnt) {
+  __shared__ unsigned long long bits[kMaxReq];
+  __shared__ int offs[kMaxReq + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int r = wave; r < p.n_req; r += nw) {
+    const ReqPlan& q = p.r[r];
+    bool m = false;
+    if (lane < q.blk_len) m = all_rows || mask[(long)q.tok_off + q.blk_s + lane] != 0;
+    unsigned long long b = __ballot(m);
+    if (lane == 0) bits[r] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int r = 0; r < p.n_req; ++r) {
+      offs[r] = acc;
+      acc += __popcll(bits[r]);
+    }
+    offs[p.n_req] = acc;
+    *lm_count = acc;
+  }
+  __syncthreads();
+  for (int r = wave; r < p.n_req; r += nw) {
+    const ReqPlan& q = p.r[r];
+    const unsigned long long b = bits[r];
+    if (lane == 0) {
+      req_off[r] = offs[r];
+      req_cnt[r] = __popcll(b);
+    }
+    if (lane < q.blk_len && ((b >> lane) & 1ull)) {
+      const int rank = __popcll(b & ((1ull << lane) - 1ull));
+      const int pos = q.blk_s + lane;
+      lm_rows[offs[r] + rank] = q.row0 + (pos - q.pos0);
+    }
+  }
+}
+
+hipError_t lm_select_rows(const StepPlan& p, const uint8_t* mask, int all_rows, int* lm_rows,
+                          int* lm_count, int* req_lm_off, int* req_lm_cnt, hipStream_t st) {
+  hipLaunchKernelGGL(lm_select_kernel, dim3(1), dim3(1024), 0, st, p, mask, all_rows, lm_rows,
+                     lm_count, req_lm_off, req_lm_cnt);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------- tile combine --
+// conf = 1 / S, tok = lowest argmax, from the per-vocab-tile statistics; one
+// wave per row, tiles strided over lanes, then a fixed xor tree: the result
+// does not depend on scheduling.
+struct Stat { float m; float s; int i; };
+__device__ __forceinline__ Stat comb(Stat a, Stat b) {
+  Stat r;
+  r.m = fmaxf(a.m, b.m);
+  float sa = a.s == 0.f ? 0.f : a.s * __expf(a.m - r.m);
+  float sb = b.s == 0.f ? 0.f : b.s * __expf(b.m - r.m);
+  r.s = sa + sb;
+  r.i = a.m > b.m ? a.i : (b.m > a.m ? b.i : min(a.i, b.i));
+  return r;
+}
+
+__global__ void lm_combine_kernel(const float* __restrict__ pm, const float* __restrict__ ps,
+                                  const int* __restrict__ pi, int tiles, int ld,
+                                  const int* __restrict__ lm_count, float* __restrict__ conf,
+                                  int* __restrict__ tok) {
+  const int row = blockIdx.x;
+  if (row >= *lm_count) return;
+  const int lane = threadIdx.x;
+  Stat a = {-INFINITY, 0.f, 0x7fffffff};
+  for (int t = lane; t < tiles; t += 64) {
+    Stat b = {pm[(long)t * ld + row], ps[(long)t * ld + row], pi[(long)t * ld + row]};
+    a = comb(a, b);
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    Stat b;
+    b.m = __shfl_xor(a.m, o, 64);
+    b.s = __shfl_xor(a.s, o, 64);
+    b.i = __shfl_xor(a.i, o, 64);
+    a = comb(a, b);
+  }
+  if (lane == 0) {
+    conf[row] = 1.0f / a.s;
+    tok[row] = a.i;
+  }
+}
+
+hipError_t lm_combine(const float* pm, const float* ps, const int* pi, int tiles, int ld,
+                      const int* lm_count, int m_max, float* conf, int* tok, hipStream_t st) {
+  if (m_max == 0) return hipSuccess;
+  hipLaunchKernelGGL(lm_combine_kernel, dim3(m_max), dim3(64), 0, st, pm, ps, pi, tiles, ld,
+                     lm_count, conf, tok);
+  return hipGetLastError();
+}
+
+// -------------------------------------------------- threshold / unmask --
+// One wave per request, lane j = block position blk_s + j. Masked positions
+// whose confidence exceeds gamma are unmasked; if none does, the most
+// confident masked position (lowest position on ties) is unmasked alone.
+// Unmasked (pos, tok, conf) are written in ascending position order.
+__global__ __launch_bounds__(64) void unmask_kernel(
+    StepPlan p, const float* __restrict__ conf, const int* __restrict__ tok,
+    const int* __restrict__ req_lm_off, int32_t* __restrict__ tokens, uint8_t* __restrict__ mask,
+    int32_t* __restrict__ n_unmasked, int32_t* __restrict__ out_pos, int32_t* __restrict__ out_tok,
+    float* __restrict__ out_conf, float* __restrict__ blk_conf, int32_t* __restrict__ blk_tok) {
+  const int r = blockIdx.x;
+  const ReqPlan& q = p.r[r];
+  const int lane = threadIdx.x;
+  const long ti = (long)q.tok_off + q.blk_s + lane;
+  const bool in_blk = lane < q.blk_len;
+  const bool masked = in_blk && mask[ti] != 0;
+  const unsigned long long mb = __ballot(masked);
+  float c = -1.0f;
+  int t = 0;
+  if (masked) {
+    const int idx = req_lm_off[r] + __popcll(mb & ((1ull << lane) - 1ull));
+    c = conf[idx];
+    t = tok[idx];
+  }
+  bool sel = masked && c > q.gamma;
+  unsigned long long sb = __ballot(sel);
+  if (sb == 0ull && mb != 0ull) {
+    // wave argmax of c over masked lanes, lowest lane on ties
+    float bc = masked ? c : -2.0f;
+    int bl = masked ? lane : 64;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      float oc = __shfl_xor(bc, o, 64);
+      int ol = __shfl_xor(bl, o, 64);
+      if (oc > bc || (oc == bc && ol < bl)) { bc = oc; bl = ol; }
+    }
+    sel = lane == bl;
+    sb = __ballot(sel);
+  }
+  if (blk_conf) blk_conf[r * kMaxBlock + lane] = masked ? c : -1.0f;
+  if (blk_tok) blk_tok[r * kMaxBlock + lane] = masked ? t : -1;
+  if (sel) {
+    const int k = __popcll(sb & ((1ull << lane) - 1ull));
+    out_pos[r * kMaxBlock + k] = q.blk_s + lane;
+    out_tok[r * kMaxBlock + k] = t;
+    out_conf[r * kMaxBlock + k] = c;
+    tokens[ti] = t;
+    mask[ti] = 0;
+  }
+  if (lane == 0) n_unmasked[r] = __popcll(sb);
+}
+
+hipError_t unmask_select(const StepPlan& p, const float* conf, const int* tok,
+                         const int* req_lm_off, int32_t* tokens, uint8_t* mask,
+                         int32_t* n_unmasked, int32_t* out_pos, int32_t* out_tok,
+                         float* out_conf, float* blk_conf, int32_t* blk_tok, hipStream_t st) {
+  hipLaunchKernelGGL(unmask_kernel, dim3(p.n_req), dim3(64), 0, st, p, conf, tok, req_lm_off,
+                     tokens, mask, n_unmasked, out_pos, out_tok, out_conf, blk_conf, blk_tok);
+  return hipGetLastError();
+}
+
+#define INST(T)                                                                                 \
+  template hipError_t embed_rows<T>(const StepPlan&, const T*, int, int, int, const int32_t*,  \
+                                    const uint8_t*, float*, hipStream_t);                      \
+  template hipError_t rmsnorm_rows<T>(const float*, const float*, int, int, float, T*,         \
+                                      hipStream_t);                                            \
+  template hipError_t final_norm_gather<T>(const float*, const float*, const int*, const int*, \
+                                           int, int, float, T*, hipStream_t);                  \
+  template hipError_t qkv_rope_scatter<T>(const StepPlan&, const float*, int, long,            \
+                                          const float2*, int, int, int, T*, T*, T*, int,       \
+                                          hipStream_t);
+INST(bf16)
+INST(float)
+
+}  // namespace dlm

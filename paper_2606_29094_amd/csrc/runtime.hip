@@ -1,0 +1,534 @@
+// Host runtime behind include/dlm.h: argument validation, the per-step row
+// plan, KV-slot bookkeeping, workspace layout and the kernel sequence of one
+// denoising step. Device memory is always the caller's.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "../../include/dlm.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace dlm;
+
+namespace {
+
+thread_local std::string g_err;
+
+dlm_status fail(dlm_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIPCHECK(expr)                                                               \
+  do {                                                                               \
+    hipError_t e_ = (expr);                                                          \
+    if (e_ != hipSuccess)                                                            \
+      return fail(DLM_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));          \
+  } while (0)
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace
+
+struct dlm_model {
+  dlm_config cfg;
+  const void* embed;
+  const void* lm_head;
+  const float* final_norm;
+  std::vector<dlm_layer_weights> layers;
+  int num_cu;
+  size_t es;   // element size
+};
+
+struct SlotState {
+  bool valid = false;
+  int block_start = -1;
+  int seq_len = -1;
+};
+
+struct dlm_cache {
+  const dlm_model* model;
+  int n_slots;
+  int s_max;          // positions per slot (multiple of 64)
+  char* base;
+  size_t region;      // bytes of one layer's K (or V) region
+  std::vector<SlotState> slots;
+  void* k_layer(int l) const { return base + (size_t)(2 * l) * region; }
+  void* v_layer(int l) const { return base + (size_t)(2 * l + 1) * region; }
+};
+
+namespace {
+
+// Workspace layout of a step with n recomputed rows and n_req requests.
+struct Layout {
+  size_t h, a, qkv, cs, q, ao, part, act, lm_rows, lm_count, req_off, req_cnt, u, pm, ps, pi,
+      conf, tok, total;
+  int s_qkv, s_o, s_down, tiles, m_max;
+};
+
+int splits_for(const dlm_model* m, int M, int N, int K) {
+  return gemm_split_count(M, N, K, m->num_cu);
+}
+
+Layout layout(const dlm_model* m, int n, int n_req) {
+  const dlm_config& c = m->cfg;
+  Layout L{};
+  const int qkv_dim = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const int qd = c.n_q_heads * c.head_dim;
+  L.s_qkv = splits_for(m, n, qkv_dim, c.d_model);
+  L.s_o = splits_for(m, n, c.d_model, qd);
+  L.s_down = splits_for(m, n, c.d_model, c.d_ffn);
+  L.m_max = std::min(n, n_req * kMaxBlock);
+  L.tiles = lm_head_tiles(c.vocab);
+  const size_t es = m->es;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  L.h = take((size_t)n * c.d_model * 4);
+  L.a = take((size_t)n * c.d_model * es);
+  L.qkv = take((size_t)L.s_qkv * n * qkv_dim * 4);
+  L.cs = take((size_t)n * (c.head_dim / 2) * 8);
+  L.q = take((size_t)n * qd * es);
+  L.ao = take((size_t)n * qd * es);
+  L.part = take((size_t)std::max(L.s_o, L.s_down) * n * c.d_model * 4);
+  L.act = take((size_t)n * c.d_ffn * es);
+  L.lm_rows = take((size_t)std::max(L.m_max, 1) * 4);
+  L.lm_count = take(4);
+  L.req_off = take((size_t)kMaxReq * 4);
+  L.req_cnt = take((size_t)kMaxReq * 4);
+  L.u = take((size_t)std::max(L.m_max, 1) * c.d_model * es);
+  L.pm = take((size_t)L.tiles * std::max(L.m_max, 1) * 4);
+  L.ps = take((size_t)L.tiles * std::max(L.m_max, 1) * 4);
+  L.pi = take((size_t)L.tiles * std::max(L.m_max, 1) * 4);
+  L.conf = take((size_t)std::max(L.m_max, 1) * 4);
+  L.tok = take((size_t)std::max(L.m_max, 1) * 4);
+  L.total = off;
+  return L;
+}
+
+dlm_status check_config(const dlm_config* c) {
+  if (!c) return fail(DLM_EINVAL, "config is NULL");
+  if (c->dtype != DLM_F32 && c->dtype != DLM_BF16)
+    return fail(DLM_EINVAL, "dtype %d is not DLM_F32 or DLM_BF16", c->dtype);
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 ||
+      c->head_dim < 1 || c->d_ffn < 1 || c->vocab < 2)
+    return fail(DLM_EINVAL, "non-positive model dimension");
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(DLM_EUNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
+  if (c->n_q_heads % c->n_kv_heads != 0)
+    return fail(DLM_EINVAL, "n_q_heads %d is not a multiple of n_kv_heads %d", c->n_q_heads,
+                c->n_kv_heads);
+  if (c->d_model % 64 != 0)
+    return fail(DLM_EUNSUPPORTED, "d_model %d is not a multiple of 64", c->d_model);
+  if (c->d_ffn % 16 != 0)
+    return fail(DLM_EUNSUPPORTED, "d_ffn %d is not a multiple of 16", c->d_ffn);
+  if (c->mask_id < 0 || c->mask_id >= c->vocab)
+    return fail(DLM_EINVAL, "mask_id %d outside [0, vocab)", c->mask_id);
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f) || !std::isfinite(c->inv_tau) ||
+      !(c->inv_tau > 0.f))
+    return fail(DLM_EINVAL, "rms_eps, rope_theta or inv_tau out of range");
+  return DLM_OK;
+}
+
+// Row plan of one step; returns the error status (nothing enqueued yet).
+dlm_status make_plan(const dlm_model* m, const dlm_cache* c, const dlm_batch* b,
+                     const float* thr, bool force_refresh, StepPlan* p) {
+  if (!b) return fail(DLM_EINVAL, "batch is NULL");
+  if (b->n_req < 1 || b->n_req > kMaxReq)
+    return fail(DLM_EINVAL, "n_req %d outside [1, %d]", b->n_req, kMaxReq);
+  if (!b->reqs || !b->tokens || !b->mask) return fail(DLM_EINVAL, "batch pointer is NULL");
+  if (b->mode < DLM_CACHE_NONE || b->mode > DLM_CACHE_DUAL)
+    return fail(DLM_EINVAL, "cache mode %d", b->mode);
+  std::vector<char> used(c->n_slots, 0);
+  int row = 0, tile = 0, blk = 0;
+  p->n_req = b->n_req;
+  for (int r = 0; r < b->n_req; ++r) {
+    const dlm_req& q = b->reqs[r];
+    if (q.slot < 0 || q.slot >= c->n_slots)
+      return fail(DLM_EINVAL, "request %d: slot %d outside [0, %d)", r, q.slot, c->n_slots);
+    if (used[q.slot]) return fail(DLM_EINVAL, "request %d: slot %d used twice", r, q.slot);
+    used[q.slot] = 1;
+    if (q.seq_len < 1 || q.seq_len > c->s_max)
+      return fail(DLM_ESIZE, "request %d: seq_len %d outside [1, %d]", r, q.seq_len, c->s_max);
+    if (q.prompt_len < 0 || q.prompt_len > q.block_start)
+      return fail(DLM_EINVAL, "request %d: prompt_len %d vs block_start %d", r, q.prompt_len,
+                  q.block_start);
+    if (q.block_len < 1 || q.block_len > kMaxBlock || q.block_start + q.block_len > q.seq_len)
+      return fail(DLM_EINVAL, "request %d: block [%d, %d) invalid for seq_len %d", r,
+                  q.block_start, q.block_start + q.block_len, q.seq_len);
+    if (q.tok_offset < 0) return fail(DLM_EINVAL, "request %d: negative tok_offset", r);
+    if (q.flags & ~DLM_REQ_REFRESH) return fail(DLM_EINVAL, "request %d: unknown flags", r);
+    float g = 0.f;
+    if (thr) {
+      g = thr[r];
+      if (!(g >= 0.f && g <= 1.f))
+        return fail(DLM_EINVAL, "request %d: threshold outside [0, 1]", r);
+    }
+    const bool refresh = force_refresh || b->mode == DLM_CACHE_NONE || (q.flags & DLM_REQ_REFRESH);
+    int r0, r1;
+    if (refresh) {
+      r0 = 0; r1 = q.seq_len;
+    } else {
+      const SlotState& s = c->slots[q.slot];
+      if (!s.valid || s.block_start != q.block_start || s.seq_len != q.seq_len)
+        return fail(DLM_ESTATE,
+                    "request %d: cache step on slot %d whose cache is not current (refreshed at "
+                    "block %d, seq_len %d; step at block %d, seq_len %d)",
+                    r, q.slot, s.valid ? s.block_start : -1, s.valid ? s.seq_len : -1,
+                    q.block_start, q.seq_len);
+      r0 = q.block_start;
+      r1 = b->mode == DLM_CACHE_DUAL ? q.block_start + q.block_len : q.seq_len;
+    }
+    ReqPlan& rp = p->r[r];
+    rp.row0 = row;
+    rp.nrows = r1 - r0;
+    rp.pos0 = r0;
+    rp.seq_len = q.seq_len;
+    rp.slot = q.slot;
+    rp.tok_off = q.tok_offset;
+    rp.blk_s = q.block_start;
+    rp.blk_len = q.block_len;
+    rp.tile0 = tile;
+    rp.blk0 = blk;
+    rp.gamma = g;
+    row += rp.nrows;
+    tile += ceil_div(rp.nrows, kQTile);
+    blk += q.block_len;
+  }
+  p->n_rows = row;
+  p->n_tiles = tile;
+  p->n_blk = blk;
+  (void)m;
+  return DLM_OK;
+}
+
+dlm_status check_ws(const dlm_model* m, const StepPlan& p, void* ws, size_t ws_bytes,
+                    Layout* L) {
+  *L = layout(m, p.n_rows, p.n_req);
+  if (!ws) return fail(DLM_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return fail(DLM_EINVAL, "workspace is not 256-byte aligned");
+  if (ws_bytes < L->total)
+    return fail(DLM_ESIZE, "workspace of %zu bytes; this step needs %zu (%d rows)", ws_bytes,
+                L->total, p.n_rows);
+  return DLM_OK;
+}
+
+enum class Tail { Unmask, Logits, None };
+
+template <typename T>
+dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPlan& p,
+                       const Layout& L, char* ws, hipStream_t st) {
+  const dlm_config& cf = m->cfg;
+  const int d = cf.d_model, hq = cf.n_q_heads, hkv = cf.n_kv_heads, dh = cf.head_dim;
+  const int qkv_dim = (hq + 2 * hkv) * dh, qd = hq * dh, n = p.n_rows;
+  float* h = reinterpret_cast<float*>(ws + L.h);
+  T* a = reinterpret_cast<T*>(ws + L.a);
+  float* qkv = reinterpret_cast<float*>(ws + L.qkv);
+  float2* cs = reinterpret_cast<float2*>(ws + L.cs);
+  T* q = reinterpret_cast<T*>(ws + L.q);
+  T* ao = reinterpret_cast<T*>(ws + L.ao);
+  float* part = reinterpret_cast<float*>(ws + L.part);
+  T* act = reinterpret_cast<T*>(ws + L.act);
+
+  HIPCHECK(rope_table(p, dh, cf.rope_theta, cs, st));
+  HIPCHECK(embed_rows<T>(p, reinterpret_cast<const T*>(m->embed), d, cf.vocab, cf.mask_id,
+                         b->tokens, b->mask, h, st));
+  for (int l = 0; l < cf.n_layers; ++l) {
+    const dlm_layer_weights& w = m->layers[l];
+    T* kc = reinterpret_cast<T*>(c->k_layer(l));
+    T* vc = reinterpret_cast<T*>(c->v_layer(l));
+    HIPCHECK(rmsnorm_rows<T>(h, w.attn_norm, n, d, cf.rms_eps, a, st));
+    HIPCHECK(gemm_store_f32<T>(a, d, reinterpret_cast<const T*>(w.w_qkv), d, n, qkv_dim, d,
+                               L.s_qkv, qkv, qkv_dim, st));
+    HIPCHECK(qkv_rope_scatter<T>(p, qkv, L.s_qkv, (long)n * qkv_dim, cs, hq, hkv, dh, q, kc, vc,
+                                 c->s_max, st));
+    HIPCHECK(attention<T>(p, q, kc, vc, c->s_max, hq, hkv, dh, ao, st));
+    if (L.s_o == 1) {
+      HIPCHECK(gemm_add_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, h, d, st));
+    } else {
+      HIPCHECK(gemm_store_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, L.s_o,
+                                 part, d, st));
+      HIPCHECK(add_partials(part, L.s_o, (long)n * d, n, d, h, st));
+    }
+    HIPCHECK(rmsnorm_rows<T>(h, w.ffn_norm, n, d, cf.rms_eps, a, st));
+    HIPCHECK(gemm_swiglu<T>(a, d, reinterpret_cast<const T*>(w.w_gate_up), d, n, cf.d_ffn, d, act,
+                            cf.d_ffn, st));
+    if (L.s_down == 1) {
+      HIPCHECK(gemm_add_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n, d,
+                               cf.d_ffn, h, d, st));
+    } else {
+      HIPCHECK(gemm_store_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n,
+                                 d, cf.d_ffn, L.s_down, part, d, st));
+      HIPCHECK(add_partials(part, L.s_down, (long)n * d, n, d, h, st));
+    }
+  }
+  return DLM_OK;
+}
+
+template <typename T>
+dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPlan& p,
+                    const Layout& L, char* ws, Tail tail, const dlm_step_out* out,
+                    float* logits, hipStream_t st) {
+  dlm_status s = run_forward<T>(m, c, b, p, L, ws, st);
+  if (s != DLM_OK || tail == Tail::None) return s;
+  const dlm_config& cf = m->cfg;
+  const int d = cf.d_model;
+  float* h = reinterpret_cast<float*>(ws + L.h);
+  int* lm_rows = reinterpret_cast<int*>(ws + L.lm_rows);
+  int* lm_count = reinterpret_cast<int*>(ws + L.lm_count);
+  int* req_off = reinterpret_cast<int*>(ws + L.req_off);
+  int* req_cnt = reinterpret_cast<int*>(ws + L.req_cnt);
+  T* u = reinterpret_cast<T*>(ws + L.u);
+  const int m_max = p.n_blk;
+  HIPCHECK(lm_select_rows(p, b->mask, tail == Tail::Logits ? 1 : 0, lm_rows, lm_count, req_off,
+                          req_cnt, st));
+  HIPCHECK(final_norm_gather<T>(h, m->final_norm, lm_rows, lm_count, m_max, d, cf.rms_eps, u, st));
+  if (tail == Tail::Logits) {
+    HIPCHECK(gemm_scaled_f32<T>(u, d, reinterpret_cast<const T*>(m->lm_head), d, m_max, cf.vocab,
+                                d, cf.inv_tau, logits, cf.vocab, st));
+    return DLM_OK;
+  }
+  float* pm = reinterpret_cast<float*>(ws + L.pm);
+  float* ps = reinterpret_cast<float*>(ws + L.ps);
+  int* pi = reinterpret_cast<int*>(ws + L.pi);
+  float* conf = reinterpret_cast<float*>(ws + L.conf);
+  int* tok = reinterpret_cast<int*>(ws + L.tok);
+  HIPCHECK(gemm_lm_head<T>(u, d, reinterpret_cast<const T*>(m->lm_head), m_max, cf.vocab, d,
+                           cf.inv_tau, pm, ps, pi, L.m_max, st));
+  HIPCHECK(lm_combine(pm, ps, pi, L.tiles, L.m_max, lm_count, m_max, conf, tok, st));
+  HIPCHECK(unmask_select(p, conf, tok, req_off, b->tokens, b->mask, out->n_unmasked, out->pos,
+                         out->tok, out->conf, out->block_conf, out->block_tok, st));
+  return DLM_OK;
+}
+
+void mark_refreshed(dlm_cache* c, const dlm_batch* b, bool force_refresh) {
+  for (int r = 0; r < b->n_req; ++r) {
+    const dlm_req& q = b->reqs[r];
+    if (force_refresh || b->mode == DLM_CACHE_NONE || (q.flags & DLM_REQ_REFRESH)) {
+      SlotState& s = c->slots[q.slot];
+      s.valid = true;
+      s.block_start = q.block_start;
+      s.seq_len = q.seq_len;
+    }
+  }
+}
+
+dlm_status dispatch(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPlan& p,
+                    const Layout& L, void* ws, Tail tail, const dlm_step_out* out,
+                    float* logits, void* stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  char* w = reinterpret_cast<char*>(ws);
+  if (m->cfg.dtype == DLM_BF16) return run_step<bf16>(m, c, b, p, L, w, tail, out, logits, st);
+  return run_step<float>(m, c, b, p, L, w, tail, out, logits, st);
+}
+
+dlm_status check_handles(dlm_model* m, dlm_cache* c) {
+  if (!m) return fail(DLM_EINVAL, "model is NULL");
+  if (!c) return fail(DLM_EINVAL, "cache is NULL");
+  if (c->model != m) return fail(DLM_EINVAL, "cache was allocated for another model");
+  return DLM_OK;
+}
+
+__global__ void fill_i32_kernel(int* p, int v) { *p = v; }
+
+}  // namespace
+
+extern "C" {
+
+const char* dlm_last_error(void) { return g_err.c_str(); }
+
+dlm_status dlm_load_weights(const dlm_config* cfg, const dlm_weights* w, dlm_model** out) {
+  g_err.clear();
+  if (!out) return fail(DLM_EINVAL, "out is NULL");
+  *out = nullptr;
+  dlm_status s = check_config(cfg);
+  if (s != DLM_OK) return s;
+  if (!w || !w->embed || !w->lm_head || !w->final_norm || !w->layers)
+    return fail(DLM_EINVAL, "weights pointer is NULL");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const dlm_layer_weights& lw = w->layers[l];
+    if (!lw.attn_norm || !lw.w_qkv || !lw.w_o || !lw.ffn_norm || !lw.w_gate_up || !lw.w_down)
+      return fail(DLM_EINVAL, "layer %d: weight pointer is NULL", l);
+  }
+  dlm_model* m = new dlm_model();
+  m->cfg = *cfg;
+  m->embed = w->embed;
+  m->lm_head = w->lm_head;
+  m->final_norm = w->final_norm;
+  m->layers.assign(w->layers, w->layers + cfg->n_layers);
+  m->es = cfg->dtype == DLM_BF16 ? 2 : 4;
+  int dev = 0, cu = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cu > 0)
+    m->num_cu = cu;
+  else
+    m->num_cu = 256;
+  (void)hipGetLastError();
+  *out = m;
+  return DLM_OK;
+}
+
+void dlm_model_destroy(dlm_model* m) { delete m; }
+
+dlm_status dlm_workspace_bytes(const dlm_model* m, int32_t max_rows, int32_t max_reqs,
+                               size_t* out_bytes) {
+  g_err.clear();
+  if (!m || !out_bytes) return fail(DLM_EINVAL, "NULL argument");
+  if (max_rows < 1 || max_reqs < 1 || max_reqs > kMaxReq)
+    return fail(DLM_EINVAL, "max_rows %d / max_reqs %d out of range", max_rows, max_reqs);
+  // split counts grow as rows shrink: take the largest layout over row counts
+  size_t best = 0;
+  for (int n = 1; n <= max_rows; n = n < 64 ? n + 1 : n + 16)
+    best = std::max(best, layout(m, n, max_reqs).total);
+  best = std::max(best, layout(m, max_rows, max_reqs).total);
+  *out_bytes = best;
+  return DLM_OK;
+}
+
+dlm_status dlm_kv_cache_alloc(const dlm_model* m, int32_t n_slots, int32_t max_seq_len,
+                              void* dev_buf, size_t buf_bytes, size_t* required_bytes,
+                              dlm_cache** out) {
+  g_err.clear();
+  if (!m) return fail(DLM_EINVAL, "model is NULL");
+  if (n_slots < 1) return fail(DLM_EINVAL, "n_slots %d < 1", n_slots);
+  if (max_seq_len < 1 || max_seq_len > DLM_MAX_SEQ)
+    return fail(DLM_ESIZE, "max_seq_len %d outside [1, %d]", max_seq_len, DLM_MAX_SEQ);
+  const dlm_config& c = m->cfg;
+  const int s_max = (int)align_up(max_seq_len, 64);
+  const size_t region = (size_t)n_slots * c.n_kv_heads * s_max * c.head_dim * m->es;
+  const size_t need = region * 2 * c.n_layers;
+  if (required_bytes) *required_bytes = need;
+  if (!dev_buf) {
+    if (out) *out = nullptr;
+    return DLM_OK;
+  }
+  if (!out) return fail(DLM_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (buf_bytes < need) return fail(DLM_ESIZE, "cache buffer %zu bytes < %zu", buf_bytes, need);
+  if (reinterpret_cast<uintptr_t>(dev_buf) % 256 != 0)
+    return fail(DLM_EINVAL, "cache buffer is not 256-byte aligned");
+  dlm_cache* k = new dlm_cache();
+  k->model = m;
+  k->n_slots = n_slots;
+  k->s_max = s_max;
+  k->base = reinterpret_cast<char*>(dev_buf);
+  k->region = region;
+  k->slots.assign(n_slots, SlotState{});
+  *out = k;
+  return DLM_OK;
+}
+
+void dlm_cache_destroy(dlm_cache* c) { delete c; }
+
+dlm_status dlm_cache_invalidate(dlm_cache* c, int32_t slot) {
+  g_err.clear();
+  if (!c) return fail(DLM_EINVAL, "cache is NULL");
+  if (slot < 0 || slot >= c->n_slots) return fail(DLM_EINVAL, "slot %d out of range", slot);
+  c->slots[slot] = SlotState{};
+  return DLM_OK;
+}
+
+dlm_status dlm_denoise_step(dlm_model* m, dlm_cache* c, const dlm_batch* b,
+                            const float* thresholds, const dlm_step_out* out, void* workspace,
+                            size_t ws_bytes, void* stream) {
+  g_err.clear();
+  dlm_status s = check_handles(m, c);
+  if (s != DLM_OK) return s;
+  if (!thresholds) return fail(DLM_EINVAL, "thresholds is NULL");
+  if (!out || !out->n_unmasked || !out->pos || !out->tok || !out->conf)
+    return fail(DLM_EINVAL, "step output pointer is NULL");
+  StepPlan p;
+  s = make_plan(m, c, b, thresholds, false, &p);
+  if (s != DLM_OK) return s;
+  Layout L;
+  s = check_ws(m, p, workspace, ws_bytes, &L);
+  if (s != DLM_OK) return s;
+  s = dispatch(m, c, b, p, L, workspace, Tail::Unmask, out, nullptr, stream);
+  if (s == DLM_OK) mark_refreshed(c, b, false);
+  return s;
+}
+
+dlm_status dlm_cache_refresh(dlm_model* m, dlm_cache* c, const dlm_batch* b, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  g_err.clear();
+  dlm_status s = check_handles(m, c);
+  if (s != DLM_OK) return s;
+  StepPlan p;
+  s = make_plan(m, c, b, nullptr, true, &p);
+  if (s != DLM_OK) return s;
+  Layout L;
+  s = check_ws(m, p, workspace, ws_bytes, &L);
+  if (s != DLM_OK) return s;
+  s = dispatch(m, c, b, p, L, workspace, Tail::None, nullptr, nullptr, stream);
+  if (s == DLM_OK) mark_refreshed(c, b, true);
+  return s;
+}
+
+dlm_status dlm_debug_logits(dlm_model* m, dlm_cache* c, const dlm_batch* b, float* logits_out,
+                            void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  dlm_status s = check_handles(m, c);
+  if (s != DLM_OK) return s;
+  if (!logits_out) return fail(DLM_EINVAL, "logits_out is NULL");
+  StepPlan p;
+  s = make_plan(m, c, b, nullptr, false, &p);
+  if (s != DLM_OK) return s;
+  Layout L;
+  s = check_ws(m, p, workspace, ws_bytes, &L);
+  if (s != DLM_OK) return s;
+  s = dispatch(m, c, b, p, L, workspace, Tail::Logits, nullptr, logits_out, stream);
+  if (s == DLM_OK) mark_refreshed(c, b, false);
+  return s;
+}
+
+dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows, float* conf,
+                               int32_t* tok, void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (!m) return fail(DLM_EINVAL, "model is NULL");
+  if (!u_rows || !conf || !tok) return fail(DLM_EINVAL, "NULL buffer");
+  if (m_rows < 1) return fail(DLM_EINVAL, "m_rows %d < 1", m_rows);
+  if (!workspace) return fail(DLM_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(DLM_EINVAL, "workspace is not 256-byte aligned");
+  const int tiles = lm_head_tiles(m->cfg.vocab);
+  const size_t stat = align_up((size_t)tiles * m_rows * 4, 256);
+  const size_t need = 3 * stat + 256;
+  if (ws_bytes < need) return fail(DLM_ESIZE, "workspace of %zu bytes; needs %zu", ws_bytes, need);
+  char* w = reinterpret_cast<char*>(workspace);
+  float* pm = reinterpret_cast<float*>(w);
+  float* ps = reinterpret_cast<float*>(w + stat);
+  int* pi = reinterpret_cast<int*>(w + 2 * stat);
+  int* cnt = reinterpret_cast<int*>(w + 3 * stat);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(1), 0, st, cnt, (int)m_rows);
+  HIPCHECK(hipGetLastError());
+  const dlm_config& cf = m->cfg;
+  if (cf.dtype == DLM_BF16) {
+    HIPCHECK(gemm_lm_head<bf16>(reinterpret_cast<const bf16*>(u_rows), cf.d_model,
+                                reinterpret_cast<const bf16*>(m->lm_head), m_rows, cf.vocab,
+                                cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, st));
+  } else {
+    HIPCHECK(gemm_lm_head<float>(reinterpret_cast<const float*>(u_rows), cf.d_model,
+                                 reinterpret_cast<const float*>(m->lm_head), m_rows, cf.vocab,
+                                 cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, st));
+  }
+  HIPCHECK(lm_combine(pm, ps, pi, tiles, m_rows, cnt, m_rows, conf, tok, st));
+  return DLM_OK;
+}
+
+}  // extern "C"

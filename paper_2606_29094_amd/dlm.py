@@ -1,0 +1,197 @@
+"""ctypes binding of libdlm.so: the same entry points as include/dlm.h.
+
+Argument marshalling only: torch tensors supply device memory and streams,
+every step of the computation runs in the library's HIP kernels. If the
+library is not built the import of any entry point raises; there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_float, c_int32, c_size_t, c_uint8, c_void_p
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdlm.so")
+
+DLM_OK, DLM_EINVAL, DLM_ESIZE, DLM_EHIP, DLM_ESTATE, DLM_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+DLM_F32, DLM_BF16 = 0, 1
+DLM_CACHE_NONE, DLM_CACHE_PREFIX, DLM_CACHE_DUAL = 0, 1, 2
+DLM_MAX_BLOCK, DLM_MAX_REQ, DLM_MAX_SEQ = 64, 64, 8192
+DLM_REQ_REFRESH = 1
+MODES = {"none": DLM_CACHE_NONE, "prefix": DLM_CACHE_PREFIX, "dual": DLM_CACHE_DUAL}
+
+EXPORTS = ["dlm_load_weights", "dlm_model_destroy", "dlm_workspace_bytes",
+           "dlm_kv_cache_alloc", "dlm_cache_destroy", "dlm_cache_invalidate",
+           "dlm_denoise_step", "dlm_cache_refresh", "dlm_debug_logits",
+           "dlm_head_confidence", "dlm_last_error"]
+
+
+class DlmConfig(ctypes.Structure):
+    _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_q_heads", c_int32),
+                ("n_kv_heads", c_int32), ("head_dim", c_int32), ("d_ffn", c_int32),
+                ("vocab", c_int32), ("mask_id", c_int32), ("rms_eps", c_float),
+                ("rope_theta", c_float), ("inv_tau", c_float), ("dtype", c_int32)]
+
+
+class DlmLayerWeights(ctypes.Structure):
+    _fields_ = [("attn_norm", c_void_p), ("w_qkv", c_void_p), ("w_o", c_void_p),
+                ("ffn_norm", c_void_p), ("w_gate_up", c_void_p), ("w_down", c_void_p)]
+
+
+class DlmWeights(ctypes.Structure):
+    _fields_ = [("embed", c_void_p), ("lm_head", c_void_p), ("final_norm", c_void_p),
+                ("layers", POINTER(DlmLayerWeights))]
+
+
+class DlmReq(ctypes.Structure):
+    _fields_ = [("slot", c_int32), ("seq_len", c_int32), ("prompt_len", c_int32),
+                ("block_start", c_int32), ("block_len", c_int32), ("tok_offset", c_int32),
+                ("flags", c_int32)]
+
+
+class DlmBatch(ctypes.Structure):
+    _fields_ = [("n_req", c_int32), ("reqs", POINTER(DlmReq)), ("tokens", c_void_p),
+                ("mask", c_void_p), ("mode", c_int32)]
+
+
+class DlmStepOut(ctypes.Structure):
+    _fields_ = [("n_unmasked", c_void_p), ("pos", c_void_p), ("tok", c_void_p),
+                ("conf", c_void_p), ("block_conf", c_void_p), ("block_tok", c_void_p)]
+
+
+class DlmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"dlm status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+                               "(there is no fallback implementation)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.dlm_load_weights.argtypes = [POINTER(DlmConfig), POINTER(DlmWeights), POINTER(c_void_p)]
+        L.dlm_model_destroy.argtypes = [c_void_p]
+        L.dlm_model_destroy.restype = None
+        L.dlm_workspace_bytes.argtypes = [c_void_p, c_int32, c_int32, POINTER(c_size_t)]
+        L.dlm_kv_cache_alloc.argtypes = [c_void_p, c_int32, c_int32, c_void_p, c_size_t,
+                                         POINTER(c_size_t), POINTER(c_void_p)]
+        L.dlm_cache_destroy.argtypes = [c_void_p]
+        L.dlm_cache_destroy.restype = None
+        L.dlm_cache_invalidate.argtypes = [c_void_p, c_int32]
+        L.dlm_denoise_step.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), POINTER(c_float),
+                                       POINTER(DlmStepOut), c_void_p, c_size_t, c_void_p]
+        L.dlm_cache_refresh.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), c_void_p,
+                                        c_size_t, c_void_p]
+        L.dlm_debug_logits.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), c_void_p,
+                                       c_void_p, c_size_t, c_void_p]
+        L.dlm_head_confidence.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
+                                          c_void_p, c_size_t, c_void_p]
+        L.dlm_last_error.argtypes = []
+        L.dlm_last_error.restype = ctypes.c_char_p
+        for name in ["dlm_load_weights", "dlm_workspace_bytes", "dlm_kv_cache_alloc",
+                     "dlm_cache_invalidate", "dlm_denoise_step", "dlm_cache_refresh",
+                     "dlm_debug_logits", "dlm_head_confidence"]:
+            getattr(L, name).restype = c_int32
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().dlm_last_error().decode()
+
+
+def check(status: int):
+    if status != DLM_OK:
+        raise DlmError(status, last_error())
+
+
+def _ptr(t):
+    return None if t is None else c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is not None:
+        return c_void_p(stream)
+    import torch
+    return c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+# ------------------------------------------------------------- entry points
+def load_weights(cfg: DlmConfig, weights: DlmWeights) -> c_void_p:
+    h = c_void_p()
+    check(lib().dlm_load_weights(ctypes.byref(cfg), ctypes.byref(weights), ctypes.byref(h)))
+    return h
+
+
+def model_destroy(h):
+    lib().dlm_model_destroy(h)
+
+
+def workspace_bytes(model, max_rows: int, max_reqs: int) -> int:
+    out = c_size_t()
+    check(lib().dlm_workspace_bytes(model, max_rows, max_reqs, ctypes.byref(out)))
+    return out.value
+
+
+def kv_cache_alloc(model, n_slots: int, max_seq_len: int, dev_buf=None, buf_bytes: int = 0):
+    """Returns (cache handle or None, required bytes)."""
+    req = c_size_t()
+    h = c_void_p()
+    check(lib().dlm_kv_cache_alloc(model, n_slots, max_seq_len, _ptr(dev_buf), buf_bytes,
+                                   ctypes.byref(req), ctypes.byref(h)))
+    return (h if dev_buf is not None else None), req.value
+
+
+def cache_destroy(h):
+    lib().dlm_cache_destroy(h)
+
+
+def cache_invalidate(cache, slot: int):
+    check(lib().dlm_cache_invalidate(cache, slot))
+
+
+def make_batch(reqs, tokens, mask, mode: int):
+    arr = (DlmReq * len(reqs))(*reqs)
+    b = DlmBatch(len(reqs), ctypes.cast(arr, POINTER(DlmReq)), tokens.data_ptr(),
+                 mask.data_ptr(), mode)
+    b._keep = arr
+    return b
+
+
+def make_step_out(n_unmasked, pos, tok, conf, block_conf=None, block_tok=None):
+    return DlmStepOut(n_unmasked.data_ptr(), pos.data_ptr(), tok.data_ptr(), conf.data_ptr(),
+                      None if block_conf is None else block_conf.data_ptr(),
+                      None if block_tok is None else block_tok.data_ptr())
+
+
+def denoise_step(model, cache, batch: DlmBatch, thresholds, out: DlmStepOut, workspace,
+                 stream=None):
+    thr = (c_float * batch.n_req)(*[float(t) for t in thresholds])
+    check(lib().dlm_denoise_step(model, cache, ctypes.byref(batch), thr, ctypes.byref(out),
+                                 _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 _stream(stream)))
+
+
+def cache_refresh(model, cache, batch: DlmBatch, workspace, stream=None):
+    check(lib().dlm_cache_refresh(model, cache, ctypes.byref(batch), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def debug_logits(model, cache, batch: DlmBatch, logits_out, workspace, stream=None):
+    check(lib().dlm_debug_logits(model, cache, ctypes.byref(batch), _ptr(logits_out),
+                                 _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 _stream(stream)))
+
+
+def head_confidence(model, u_rows, m_rows: int, conf, tok, workspace, stream=None):
+    check(lib().dlm_head_confidence(model, _ptr(u_rows), m_rows, _ptr(conf), _ptr(tok),
+                                    _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(),
+                                    _stream(stream)))

@@ -1,0 +1,271 @@
+"""Host driver of the denoising step: device buffers, request bookkeeping and
+the block-by-block generation loop around ``dlm_denoise_step``.
+
+Block protocol (paper, "Support for Approximate Caching" and "Supporting
+Approximate KV Caching"): the generation positions are split into blocks that
+are denoised in order; with a cache, the first step of every block is a
+recompute step that rewrites the request's slot, the following steps of the
+block are cache steps; a request moves to the next block once its active block
+has no [MASK] left, and is done after its last block. The host learns how many
+positions a step unmasked from one small device-to-host copy per step.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import dlm
+
+
+# ------------------------------------------------------------------ model
+@dataclass
+class ModelShape:
+    n_layers: int
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_ffn: int
+    vocab: int
+    dtype: str                 # "f32" | "bf16"
+    rms_eps: float = 1e-5
+    rope_theta: float = 10000.0
+    mask_id: Optional[int] = None
+
+    @property
+    def qkv_dim(self):
+        return (self.n_q_heads + 2 * self.n_kv_heads) * self.head_dim
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    @staticmethod
+    def of(cfg) -> "ModelShape":
+        return ModelShape(cfg.n_layers, cfg.d_model, cfg.n_q_heads, cfg.n_kv_heads,
+                          cfg.head_dim, cfg.d_ffn, cfg.vocab, cfg.dtype, cfg.rms_eps,
+                          cfg.rope_theta, cfg.vocab - 1)
+
+
+class DeviceModel:
+    """Caller-owned device weights plus the library's model handle.
+
+    ``tensors``: embed, lm_head, final_norm and ``layers`` (list of dicts with
+    attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down), torch CUDA tensors in
+    the layouts of include/dlm.h."""
+
+    def __init__(self, shape: ModelShape, tensors: dict, inv_tau: float):
+        self.shape = shape
+        self.tensors = tensors
+        self.inv_tau = float(inv_tau)
+        self._layer_arr = (dlm.DlmLayerWeights * shape.n_layers)(*[
+            dlm.DlmLayerWeights(l["attn_norm"].data_ptr(), l["w_qkv"].data_ptr(),
+                                l["w_o"].data_ptr(), l["ffn_norm"].data_ptr(),
+                                l["w_gate_up"].data_ptr(), l["w_down"].data_ptr())
+            for l in tensors["layers"]])
+        self.weights = dlm.DlmWeights(tensors["embed"].data_ptr(), tensors["lm_head"].data_ptr(),
+                                      tensors["final_norm"].data_ptr(),
+                                      self._layer_arr)
+        mask_id = shape.vocab - 1 if shape.mask_id is None else shape.mask_id
+        self.config = dlm.DlmConfig(shape.n_layers, shape.d_model, shape.n_q_heads,
+                                    shape.n_kv_heads, shape.head_dim, shape.d_ffn, shape.vocab,
+                                    mask_id, shape.rms_eps, shape.rope_theta, self.inv_tau,
+                                    dlm.DLM_BF16 if shape.dtype == "bf16" else dlm.DLM_F32)
+        self.handle = dlm.load_weights(self.config, self.weights)
+
+    def close(self):
+        if self.handle:
+            dlm.model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------- requests
+@dataclass
+class Request:
+    prompt: np.ndarray
+    gen_len: int
+    block: int
+    threshold: float
+    slot: int = -1
+    tok_offset: int = 0
+    k: int = 0                         # active block index
+    masked_in_block: int = 0
+    refreshed_block: int = -1          # block_start of the last recompute step
+    steps: int = 0
+    unmasked: int = 0
+
+    @property
+    def prompt_len(self):
+        return len(self.prompt)
+
+    @property
+    def seq_len(self):
+        return len(self.prompt) + self.gen_len
+
+    @property
+    def block_start(self):
+        return self.prompt_len + self.k * self.block
+
+    @property
+    def block_len(self):
+        return min(self.block, self.seq_len - self.block_start)
+
+    @property
+    def done(self):
+        return self.k * self.block >= self.gen_len
+
+
+class Engine:
+    """Slots, workspace and packed token/mask buffers for a fixed set of slots."""
+
+    def __init__(self, model: DeviceModel, n_slots: int, max_seq_len: int, mode: str,
+                 max_rows: Optional[int] = None, device="cuda:0"):
+        self.model = model
+        self.mode = mode
+        self.mode_id = dlm.MODES[mode]
+        self.device = torch.device(device)
+        self.n_slots = n_slots
+        self.max_seq_len = max_seq_len
+        _, need = dlm.kv_cache_alloc(model.handle, n_slots, max_seq_len)
+        self.cache_buf = torch.empty(need, dtype=torch.uint8, device=self.device)
+        self.cache, _ = dlm.kv_cache_alloc(model.handle, n_slots, max_seq_len, self.cache_buf,
+                                           need)
+        if max_rows is None:
+            max_rows = n_slots * max_seq_len
+        self.max_rows = max_rows
+        ws = dlm.workspace_bytes(model.handle, max_rows, min(n_slots, dlm.DLM_MAX_REQ))
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=self.device)
+        self.tokens = torch.zeros(n_slots * max_seq_len, dtype=torch.int32, device=self.device)
+        self.mask = torch.zeros(n_slots * max_seq_len, dtype=torch.uint8, device=self.device)
+        R = n_slots
+        B = dlm.DLM_MAX_BLOCK
+        self.n_unmasked = torch.zeros(R, dtype=torch.int32, device=self.device)
+        self.out_pos = torch.zeros(R * B, dtype=torch.int32, device=self.device)
+        self.out_tok = torch.zeros(R * B, dtype=torch.int32, device=self.device)
+        self.out_conf = torch.zeros(R * B, dtype=torch.float32, device=self.device)
+        self.block_conf = torch.zeros(R * B, dtype=torch.float32, device=self.device)
+        self.block_tok = torch.zeros(R * B, dtype=torch.int32, device=self.device)
+        self.host_n = torch.zeros(R, dtype=torch.int32).pin_memory()
+        self.step_out = dlm.make_step_out(self.n_unmasked, self.out_pos, self.out_tok,
+                                          self.out_conf, self.block_conf, self.block_tok)
+        self.free_slots = list(range(n_slots))[::-1]
+
+    def close(self):
+        if getattr(self, "cache", None):
+            dlm.cache_destroy(self.cache)
+            self.cache = None
+
+    # ---- admission
+    def admit(self, req: Request, mask_id: int):
+        if req.seq_len > self.max_seq_len:
+            raise ValueError("request longer than a slot")
+        req.slot = self.free_slots.pop()
+        req.tok_offset = req.slot * self.max_seq_len
+        toks = np.concatenate([np.asarray(req.prompt, np.int32),
+                               np.full(req.gen_len, mask_id, np.int32)])
+        msk = np.concatenate([np.zeros(req.prompt_len, np.uint8), np.ones(req.gen_len, np.uint8)])
+        o = req.tok_offset
+        self.tokens[o:o + req.seq_len].copy_(torch.from_numpy(toks))
+        self.mask[o:o + req.seq_len].copy_(torch.from_numpy(msk))
+        req.k = 0
+        req.masked_in_block = req.block_len
+        req.refreshed_block = -1
+        dlm.cache_invalidate(self.cache, req.slot)
+
+    def release(self, req: Request):
+        self.free_slots.append(req.slot)
+        req.slot = -1
+
+    def set_state(self, req: Request, tokens: np.ndarray, mask: np.ndarray, k: int):
+        """Overwrite a request's tokens/mask/block (teacher forcing in tests)."""
+        o = req.tok_offset
+        self.tokens[o:o + req.seq_len].copy_(torch.from_numpy(np.asarray(tokens, np.int32)))
+        self.mask[o:o + req.seq_len].copy_(torch.from_numpy(np.asarray(mask, np.uint8)))
+        req.k = k
+        if not req.done:
+            s = req.block_start
+            req.masked_in_block = int(np.asarray(mask[s:s + req.block_len]).sum())
+
+    # ---- one step
+    def dlm_reqs(self, reqs: List[Request], force_refresh: bool = False):
+        out = []
+        for r in reqs:
+            s = r.block_start
+            refresh = force_refresh or self.mode_id == dlm.DLM_CACHE_NONE or r.refreshed_block != s
+            out.append(dlm.DlmReq(r.slot, r.seq_len, r.prompt_len, s, r.block_len, r.tok_offset,
+                                  dlm.DLM_REQ_REFRESH if refresh else 0))
+        return out
+
+    def enqueue_step(self, reqs: List[Request], stream=None):
+        dreqs = self.dlm_reqs(reqs)
+        batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id)
+        dlm.denoise_step(self.model.handle, self.cache, batch, [r.threshold for r in reqs],
+                         self.step_out, self.workspace, stream)
+        for r, d in zip(reqs, dreqs):
+            if d.flags & dlm.DLM_REQ_REFRESH:
+                r.refreshed_block = r.block_start
+        return dreqs
+
+    def finish_step(self, reqs: List[Request], stream=None):
+        """Read the unmask counts back and advance blocks (synchronises)."""
+        n = len(reqs)
+        self.host_n[:n].copy_(self.n_unmasked[:n], non_blocking=True)
+        torch.cuda.current_stream().synchronize() if stream is None else \
+            torch.cuda.ExternalStream(stream).synchronize()
+        counts = self.host_n[:n].tolist()
+        for r, c in zip(reqs, counts):
+            r.steps += 1
+            r.unmasked += c
+            r.masked_in_block -= c
+            if r.masked_in_block <= 0:
+                r.k += 1
+                if not r.done:
+                    r.masked_in_block = r.block_len
+        return counts
+
+    def step(self, reqs: List[Request], stream=None):
+        self.enqueue_step(reqs, stream)
+        return self.finish_step(reqs, stream)
+
+    def debug_logits(self, reqs: List[Request]):
+        dreqs = self.dlm_reqs(reqs)
+        nblk = sum(d.block_len for d in dreqs)
+        out = torch.empty(nblk, self.model.shape.vocab, dtype=torch.float32, device=self.device)
+        batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id)
+        dlm.debug_logits(self.model.handle, self.cache, batch, out, self.workspace)
+        for r, d in zip(reqs, dreqs):
+            if d.flags & dlm.DLM_REQ_REFRESH:
+                r.refreshed_block = r.block_start
+        return out
+
+    def refresh(self, reqs: List[Request]):
+        dreqs = self.dlm_reqs(reqs, force_refresh=True)
+        batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id)
+        dlm.cache_refresh(self.model.handle, self.cache, batch, self.workspace)
+        for r in reqs:
+            r.refreshed_block = r.block_start
+
+    def read_state(self, req: Request):
+        o = req.tok_offset
+        return (self.tokens[o:o + req.seq_len].cpu().numpy().astype(np.int64),
+                self.mask[o:o + req.seq_len].cpu().numpy().astype(bool))
+
+    def read_outputs(self, n_req: int):
+        B = dlm.DLM_MAX_BLOCK
+        return {
+            "n": self.n_unmasked[:n_req].cpu().numpy(),
+            "pos": self.out_pos[:n_req * B].view(n_req, B).cpu().numpy(),
+            "tok": self.out_tok[:n_req * B].view(n_req, B).cpu().numpy(),
+            "conf": self.out_conf[:n_req * B].view(n_req, B).cpu().numpy(),
+            "block_conf": self.block_conf[:n_req * B].view(n_req, B).cpu().numpy(),
+            "block_tok": self.block_tok[:n_req * B].view(n_req, B).cpu().numpy(),
+        }
