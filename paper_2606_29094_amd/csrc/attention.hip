@@ -11,7 +11,8 @@
 // cross-lane steps, and the probabilities feed O^T = V^T P^T directly as the B
 // operand (the key order inside the 32-wide k step is permuted identically in
 // A and B, which leaves the sum unchanged). fp32 softmax, exp2 with the scale
-// folded in, P rounded to bf16 for the PV product, output rounded to bf16.
+// folded in; P enters the PV product as the sum of two bf16 terms (about 16
+// significant bits), the output is rounded to bf16.
 //
 // fp32 path: a plain per-query-row kernel (one lane per query row) over LDS
 // tiles; it serves the small fp32 model.
@@ -138,21 +139,25 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* 
 
     // O^T += V^T P^T over two 32-key steps; B operand slot 8g+e <-> key
     // 32*j + (e < 4 ? 4g + e : 16 + 4g + e - 4)
+    // P = P_hi + P_lo with both terms bf16: the product with the bf16 values
+    // keeps about 16 bits of P instead of 8 (two MFMAs per block).
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      bf16x8 pb;
+      bf16x8 ph, pl;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        pb[e] = (bf16)sblk[2 * j][e];
-        pb[4 + e] = (bf16)sblk[2 * j + 1][e];
+      for (int e = 0; e < 8; ++e) {
+        const float pv = e < 4 ? sblk[2 * j][e] : sblk[2 * j + 1][e - 4];
+        ph[e] = (bf16)pv;
+        pl[e] = (bf16)(pv - (float)ph[e]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const bf16* vrow = vs + (db * 16 + (lane & 15)) * VS + 32 * j + 4 * g;
         const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
         const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
-        const u32x4 a = u32x4{lo[0], lo[1], hi[0], hi[1]};
-        o[db] = mfma16_bf16(__builtin_bit_cast(bf16x8, a), pb, o[db]);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+        o[db] = mfma16_bf16(a, ph, o[db]);
+        o[db] = mfma16_bf16(a, pl, o[db]);
       }
     }
   }

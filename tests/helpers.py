@@ -18,6 +18,84 @@ from paper_2606_29094_amd import engine
 # confidences are within 1e-3 (the position may differ).
 LOGIT_TOL = {"bf16": 2e-2, "f32": 1e-4}
 CONF_TOL = 1e-3
+# bf16 end to end (forward + head): the fp64 oracle rounds to bf16 at the same
+# storage points but cannot reproduce the roundings the GPU takes from fp32
+# sums; every divergent rounding is a 2^-8 step and the calibrated 1/tau
+# (about 10) scales the resulting logit differences. The confidence is then
+# checked against what the row's own logit error allows: if every scaled logit
+# of a row is within eta of the oracle's, S = sum exp(z - max z) moves by at
+# most a factor exp(2 eta), so |conf_gpu - conf_ref| <= conf_ref (exp(2 eta) - 1)
+# (plus the 1e-3 of the confidence computation itself). The logits must meet
+# LOGIT_TOL first; the tight 1e-3 bound alone is checked where the head's
+# inputs are identical (dlm_head_confidence).
+
+
+def conf_bound(conf_ref, eta):
+    return np.asarray(conf_ref) * np.expm1(2.0 * np.asarray(eta)) + CONF_TOL
+
+
+def gpu_step_with_logits(eng, reqs):
+    """Scaled logits of every active-block row for the step about to run,
+    then the step itself with the same recompute/cache flags."""
+    saved = [r.refreshed_block for r in reqs]
+    z = eng.debug_logits(reqs).cpu().numpy()
+    for r, s in zip(reqs, saved):
+        r.refreshed_block = s
+    starts = [r.block_start for r in reqs]
+    lens = [r.block_len for r in reqs]
+    eng.step(reqs)
+    out = eng.read_outputs(len(reqs))
+    rows, off = [], 0
+    for L in lens:
+        rows.append(z[off:off + L])
+        off += L
+    return rows, out, starts
+
+
+def check_step_e2e(res, out_r, blk_start, gamma, z_gpu_blk, dtype="bf16"):
+    """Compare one request's GPU step with the oracle StepResult ``res``
+    (computed with keep_logits). Returns (max logit err, max conf err, exempt)."""
+    A = res.masked_positions
+    if len(A) == 0:
+        assert int(out_r["n"]) == 0
+        return 0.0, 0.0, 0
+    zg = z_gpu_blk[A - blk_start]
+    zr = res.logits
+    lerr = logit_err(zg, zr)
+    assert lerr < LOGIT_TOL[dtype], lerr
+    eta = np.abs(zg - zr).max(axis=1)
+    bound = conf_bound(res.masked_conf, eta)
+    bc = out_r["block_conf"][A - blk_start]
+    cerr = np.abs(bc - res.masked_conf)
+    assert np.all(cerr <= bound), (cerr.max(), bound[np.argmax(cerr - bound)])
+    # tokens: equal unless the oracle's top-2 scaled logits are within 2 eta
+    bt = out_r["block_tok"][A - blk_start]
+    assert np.all((bt == res.masked_tok) | (top2_gap(zr) <= 2 * eta))
+    return lerr, float(cerr.max()), check_decisions(A, res.masked_conf, bound, gamma, out_r,
+                                                     set(res.positions.tolist()))
+
+
+def check_decisions(A, conf_ref, bound, gamma, out_r, want):
+    """Unmask decisions given confidence intervals [conf_ref - bound, conf_ref + bound].
+
+    Positions certainly above the threshold must be unmasked, positions
+    certainly not above it must not be (unless forced); a forced single unmask
+    must pick a position whose interval reaches the top interval. Returns the
+    number of positions where the GPU and the oracle differ (all exempt)."""
+    n = int(out_r["n"])
+    got = set(out_r["pos"][:n].tolist())
+    assert len(got) == n and n >= (1 if len(A) else 0)
+    sure_pass = set(A[conf_ref - bound > gamma].tolist())
+    sure_fail = set(A[conf_ref + bound <= gamma].tolist())
+    top = int(np.argmax(conf_ref))
+    plausible_top = set(A[conf_ref + bound >= conf_ref[top] - bound[top]].tolist())
+    if sure_pass:
+        assert sure_pass <= got and not (got & sure_fail), (sorted(got), sorted(sure_pass))
+    elif len(got) == 1 and got <= plausible_top:
+        pass                                   # forced single unmask (or one undecided pass)
+    else:
+        assert not (got & sure_fail), (sorted(got), sorted(sure_fail))
+    return len(got ^ want)
 
 
 def host_weights(tensors, cfg) -> oracle.Weights:
