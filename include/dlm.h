@@ -71,7 +71,8 @@ enum {
 /* Request flag: this step is a recompute step (whole sequence, cache rewritten). */
 #define DLM_REQ_REFRESH 1
 
-/* Model shape. Supported: head_dim 64 or 128, d_model and d_ffn multiples of 64,
+/* Model shape. Supported: head_dim 64 or 128, d_model a multiple of 64, d_ffn a
+ * multiple of 16,
  * n_q_heads a multiple of n_kv_heads, mask_id in [0, vocab). inv_tau scales the
  * logits before the softmax (1/temperature). */
 typedef struct dlm_config {
@@ -185,6 +186,19 @@ dlm_status dlm_debug_logits(dlm_model* m, dlm_cache* c, const dlm_batch* b,
 dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
                                float* conf, int32_t* tok, void* workspace,
                                size_t ws_bytes, void* stream);
+
+/* Kernel timing. While enabled, every kernel the library enqueues for this
+ * model is bracketed by a pair of HIP events on the launch stream.
+ * dlm_profile_read waits for those events, adds their elapsed times per kernel
+ * class into out[0 .. *n_out) (at most cap entries, in first-seen order) and
+ * clears them. Timing adds two event records per kernel launch. */
+typedef struct dlm_profile_entry {
+  char name[32];          /* kernel class, e.g. "gemm_gate_up_swiglu"                  */
+  int32_t calls;          /* launches timed                                             */
+  double total_ms;        /* sum of their event-to-event times                          */
+} dlm_profile_entry;
+dlm_status dlm_profile_enable(dlm_model* m, int32_t on);
+dlm_status dlm_profile_read(dlm_model* m, dlm_profile_entry* out, int32_t cap, int32_t* n_out);
 
 /* Message for the last non-OK status on this thread ("" if none). */
 const char* dlm_last_error(void);

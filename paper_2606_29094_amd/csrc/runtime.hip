@@ -41,7 +41,55 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace
 
+// Enqueue `expr` (a launch returning hipError_t) bracketed by timing events
+// when the model's profiler is on.
+#define LAUNCH(model, stream, name, expr)                                           \
+  do {                                                                            \
+    Profiler& pf_ = (model)->prof;                                                \
+    hipEvent_t a_ = nullptr, b_ = nullptr;                                        \
+    if (pf_.on) {                                                                 \
+      a_ = pf_.take();                                                            \
+      b_ = pf_.take();                                                            \
+      if (a_) (void)hipEventRecord(a_, stream);                                   \
+    }                                                                             \
+    HIPCHECK(expr);                                                               \
+    if (pf_.on && a_ && b_) {                                                     \
+      (void)hipEventRecord(b_, stream);                                           \
+      pf_.pending.push_back({pf_.kind_of(name), a_, b_});                         \
+    }                                                                             \
+  } while (0)
+
+// Per-kernel-class event timing (dlm_profile_*).
+struct Profiler {
+  bool on = false;
+  struct Rec { int kind; hipEvent_t a, b; };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  std::vector<std::string> names;
+  int kind_of(const char* n) {
+    for (size_t i = 0; i < names.size(); ++i)
+      if (names[i] == n) return (int)i;
+    names.emplace_back(n);
+    return (int)names.size() - 1;
+  }
+  hipEvent_t take() {
+    if (pool.empty()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      return e;
+    }
+    hipEvent_t e = pool.back();
+    pool.pop_back();
+    return e;
+  }
+  ~Profiler() {
+    for (auto& r : pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+    for (auto e : pool) (void)hipEventDestroy(e);
+  }
+};
+
 struct dlm_model {
+  Profiler prof;
   dlm_config cfg;
   const void* embed;
   const void* lm_head;
@@ -245,36 +293,36 @@ dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const Ste
   float* part = reinterpret_cast<float*>(ws + L.part);
   T* act = reinterpret_cast<T*>(ws + L.act);
 
-  HIPCHECK(rope_table(p, dh, cf.rope_theta, cs, st));
-  HIPCHECK(embed_rows<T>(p, reinterpret_cast<const T*>(m->embed), d, cf.vocab, cf.mask_id,
+  LAUNCH(m, st, "rope_table", rope_table(p, dh, cf.rope_theta, cs, st));
+  LAUNCH(m, st, "embed", embed_rows<T>(p, reinterpret_cast<const T*>(m->embed), d, cf.vocab, cf.mask_id,
                          b->tokens, b->mask, h, st));
   for (int l = 0; l < cf.n_layers; ++l) {
     const dlm_layer_weights& w = m->layers[l];
     T* kc = reinterpret_cast<T*>(c->k_layer(l));
     T* vc = reinterpret_cast<T*>(c->v_layer(l));
-    HIPCHECK(rmsnorm_rows<T>(h, w.attn_norm, n, d, cf.rms_eps, a, st));
-    HIPCHECK(gemm_store_f32<T>(a, d, reinterpret_cast<const T*>(w.w_qkv), d, n, qkv_dim, d,
+    LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, w.attn_norm, n, d, cf.rms_eps, a, st));
+    LAUNCH(m, st, "gemm_qkv", gemm_store_f32<T>(a, d, reinterpret_cast<const T*>(w.w_qkv), d, n, qkv_dim, d,
                                L.s_qkv, qkv, qkv_dim, st));
-    HIPCHECK(qkv_rope_scatter<T>(p, qkv, L.s_qkv, (long)n * qkv_dim, cs, hq, hkv, dh, q, kc, vc,
+    LAUNCH(m, st, "rope_kv_write", qkv_rope_scatter<T>(p, qkv, L.s_qkv, (long)n * qkv_dim, cs, hq, hkv, dh, q, kc, vc,
                                  c->s_max, st));
-    HIPCHECK(attention<T>(p, q, kc, vc, c->s_max, hq, hkv, dh, ao, st));
+    LAUNCH(m, st, "attention", attention<T>(p, q, kc, vc, c->s_max, hq, hkv, dh, ao, st));
     if (L.s_o == 1) {
-      HIPCHECK(gemm_add_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, h, d, st));
+      LAUNCH(m, st, "gemm_o", gemm_add_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, h, d, st));
     } else {
-      HIPCHECK(gemm_store_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, L.s_o,
+      LAUNCH(m, st, "gemm_o", gemm_store_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, L.s_o,
                                  part, d, st));
-      HIPCHECK(add_partials(part, L.s_o, (long)n * d, n, d, h, st));
+      LAUNCH(m, st, "splitk_reduce", add_partials(part, L.s_o, (long)n * d, n, d, h, st));
     }
-    HIPCHECK(rmsnorm_rows<T>(h, w.ffn_norm, n, d, cf.rms_eps, a, st));
-    HIPCHECK(gemm_swiglu<T>(a, d, reinterpret_cast<const T*>(w.w_gate_up), d, n, cf.d_ffn, d, act,
+    LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, w.ffn_norm, n, d, cf.rms_eps, a, st));
+    LAUNCH(m, st, "gemm_gate_up_swiglu", gemm_swiglu<T>(a, d, reinterpret_cast<const T*>(w.w_gate_up), d, n, cf.d_ffn, d, act,
                             cf.d_ffn, st));
     if (L.s_down == 1) {
-      HIPCHECK(gemm_add_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n, d,
+      LAUNCH(m, st, "gemm_down", gemm_add_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n, d,
                                cf.d_ffn, h, d, st));
     } else {
-      HIPCHECK(gemm_store_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n,
+      LAUNCH(m, st, "gemm_down", gemm_store_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n,
                                  d, cf.d_ffn, L.s_down, part, d, st));
-      HIPCHECK(add_partials(part, L.s_down, (long)n * d, n, d, h, st));
+      LAUNCH(m, st, "splitk_reduce", add_partials(part, L.s_down, (long)n * d, n, d, h, st));
     }
   }
   return DLM_OK;
@@ -295,11 +343,11 @@ dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPl
   int* req_cnt = reinterpret_cast<int*>(ws + L.req_cnt);
   T* u = reinterpret_cast<T*>(ws + L.u);
   const int m_max = p.n_blk;
-  HIPCHECK(lm_select_rows(p, b->mask, tail == Tail::Logits ? 1 : 0, lm_rows, lm_count, req_off,
+  LAUNCH(m, st, "lm_select", lm_select_rows(p, b->mask, tail == Tail::Logits ? 1 : 0, lm_rows, lm_count, req_off,
                           req_cnt, st));
-  HIPCHECK(final_norm_gather<T>(h, m->final_norm, lm_rows, lm_count, m_max, d, cf.rms_eps, u, st));
+  LAUNCH(m, st, "final_norm", final_norm_gather<T>(h, m->final_norm, lm_rows, lm_count, m_max, d, cf.rms_eps, u, st));
   if (tail == Tail::Logits) {
-    HIPCHECK(gemm_scaled_f32<T>(u, d, reinterpret_cast<const T*>(m->lm_head), d, m_max, cf.vocab,
+    LAUNCH(m, st, "gemm_logits", gemm_scaled_f32<T>(u, d, reinterpret_cast<const T*>(m->lm_head), d, m_max, cf.vocab,
                                 d, cf.inv_tau, logits, cf.vocab, st));
     return DLM_OK;
   }
@@ -308,10 +356,10 @@ dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPl
   int* pi = reinterpret_cast<int*>(ws + L.pi);
   float* conf = reinterpret_cast<float*>(ws + L.conf);
   int* tok = reinterpret_cast<int*>(ws + L.tok);
-  HIPCHECK(gemm_lm_head<T>(u, d, reinterpret_cast<const T*>(m->lm_head), m_max, cf.vocab, d,
+  LAUNCH(m, st, "lm_head", gemm_lm_head<T>(u, d, reinterpret_cast<const T*>(m->lm_head), m_max, cf.vocab, d,
                            cf.inv_tau, pm, ps, pi, L.m_max, st));
-  HIPCHECK(lm_combine(pm, ps, pi, L.tiles, L.m_max, lm_count, m_max, conf, tok, st));
-  HIPCHECK(unmask_select(p, conf, tok, req_off, b->tokens, b->mask, out->n_unmasked, out->pos,
+  LAUNCH(m, st, "lm_combine", lm_combine(pm, ps, pi, L.tiles, L.m_max, lm_count, m_max, conf, tok, st));
+  LAUNCH(m, st, "unmask", unmask_select(p, conf, tok, req_off, b->tokens, b->mask, out->n_unmasked, out->pos,
                          out->tok, out->conf, out->block_conf, out->block_tok, st));
   return DLM_OK;
 }
@@ -384,6 +432,46 @@ dlm_status dlm_load_weights(const dlm_config* cfg, const dlm_weights* w, dlm_mod
 }
 
 void dlm_model_destroy(dlm_model* m) { delete m; }
+
+dlm_status dlm_profile_enable(dlm_model* m, int32_t on) {
+  g_err.clear();
+  if (!m) return fail(DLM_EINVAL, "model is NULL");
+  m->prof.on = on != 0;
+  return DLM_OK;
+}
+
+dlm_status dlm_profile_read(dlm_model* m, dlm_profile_entry* out, int32_t cap, int32_t* n_out) {
+  g_err.clear();
+  if (!m || !n_out || (cap > 0 && !out)) return fail(DLM_EINVAL, "NULL argument");
+  Profiler& pf = m->prof;
+  std::vector<int> calls(pf.names.size(), 0);
+  std::vector<double> ms(pf.names.size(), 0.0);
+  dlm_status st = DLM_OK;
+  for (auto& r : pf.pending) {
+    float t = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, r.a, r.b);
+    if (e != hipSuccess && st == DLM_OK)
+      st = fail(DLM_EHIP, "profile event: %s", hipGetErrorString(e));
+    calls[r.kind] += 1;
+    ms[r.kind] += t;
+    pf.pool.push_back(r.a);
+    pf.pool.push_back(r.b);
+  }
+  pf.pending.clear();
+  int n = 0;
+  for (size_t k = 0; k < pf.names.size(); ++k) {
+    if (calls[k] == 0) continue;
+    if (n < cap) {
+      snprintf(out[n].name, sizeof out[n].name, "%s", pf.names[k].c_str());
+      out[n].calls = calls[k];
+      out[n].total_ms = ms[k];
+    }
+    ++n;
+  }
+  *n_out = n < cap ? n : cap;
+  return st;
+}
 
 dlm_status dlm_workspace_bytes(const dlm_model* m, int32_t max_rows, int32_t max_reqs,
                                size_t* out_bytes) {

@@ -24,7 +24,8 @@ MODES = {"none": DLM_CACHE_NONE, "prefix": DLM_CACHE_PREFIX, "dual": DLM_CACHE_D
 EXPORTS = ["dlm_load_weights", "dlm_model_destroy", "dlm_workspace_bytes",
            "dlm_kv_cache_alloc", "dlm_cache_destroy", "dlm_cache_invalidate",
            "dlm_denoise_step", "dlm_cache_refresh", "dlm_debug_logits",
-           "dlm_head_confidence", "dlm_last_error"]
+           "dlm_head_confidence", "dlm_profile_enable", "dlm_profile_read",
+           "dlm_last_error"]
 
 
 class DlmConfig(ctypes.Structure):
@@ -60,6 +61,10 @@ class DlmStepOut(ctypes.Structure):
                 ("conf", c_void_p), ("block_conf", c_void_p), ("block_tok", c_void_p)]
 
 
+class DlmProfileEntry(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("calls", c_int32), ("total_ms", ctypes.c_double)]
+
+
 class DlmError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"dlm status {status}: {msg}")
@@ -93,11 +98,15 @@ def lib():
                                        c_void_p, c_size_t, c_void_p]
         L.dlm_head_confidence.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p]
+        L.dlm_profile_enable.argtypes = [c_void_p, c_int32]
+        L.dlm_profile_read.argtypes = [c_void_p, POINTER(DlmProfileEntry), c_int32,
+                                       POINTER(c_int32)]
         L.dlm_last_error.argtypes = []
         L.dlm_last_error.restype = ctypes.c_char_p
         for name in ["dlm_load_weights", "dlm_workspace_bytes", "dlm_kv_cache_alloc",
                      "dlm_cache_invalidate", "dlm_denoise_step", "dlm_cache_refresh",
-                     "dlm_debug_logits", "dlm_head_confidence"]:
+                     "dlm_debug_logits", "dlm_head_confidence", "dlm_profile_enable",
+                     "dlm_profile_read"]:
             getattr(L, name).restype = c_int32
         _lib = L
     return _lib
@@ -195,3 +204,15 @@ def head_confidence(model, u_rows, m_rows: int, conf, tok, workspace, stream=Non
                                     _ptr(workspace),
                                     workspace.numel() * workspace.element_size(),
                                     _stream(stream)))
+
+
+def profile_enable(model, on: bool):
+    check(lib().dlm_profile_enable(model, 1 if on else 0))
+
+
+def profile_read(model, cap: int = 64) -> dict:
+    """{kernel class: (calls, total ms)} of the launches timed since the last read."""
+    arr = (DlmProfileEntry * cap)()
+    n = c_int32()
+    check(lib().dlm_profile_read(model, arr, cap, ctypes.byref(n)))
+    return {arr[i].name.decode(): (arr[i].calls, arr[i].total_ms) for i in range(n.value)}
