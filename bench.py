@@ -38,6 +38,22 @@ def load_inv_tau(model_name: str):
         return float(json.load(f)["inv_tau"]), os.path.relpath(path, ROOT)
 
 
+def measured_traffic(kernel_class: str):
+    """HBM bytes per launch of a kernel class from the committed rocprofv3 counter
+    summary (profiles/traffic_<class>.json), or None when there is none or the
+    kernel's sources changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}.json")
+    if not os.path.exists(path):
+        return None, None
+    with open(path) as f:
+        t = json.load(f)
+    src = b"".join(open(os.path.join(ROOT, p), "rb").read() for p in t["source_files"])
+    if hashlib.sha256(src).hexdigest() != t["source_sha256"]:
+        return None, os.path.relpath(path, ROOT) + " (stale: kernel changed)"
+    return float(t["hbm_bytes_per_launch"]), os.path.relpath(path, ROOT)
+
+
 def kernel_work(shape, n_rows, seq_len, m_rows):
     """Algorithmic FLOPs and HBM bytes of one launch of each kernel class for a
     single-request no-cache step (n_rows recomputed rows, keys = seq_len,
@@ -127,6 +143,9 @@ def main():
                     help="layers of the CPU oracle sample (0 disables the CPU baseline)")
     ap.add_argument("--inv-tau", type=float, default=None,
                     help="override the stored calibrated 1/tau")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run 10 device-to-device copies of MIB MiB (calibrates the "
+                         "HBM byte counters) and exit")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-kernel event records")
     args = ap.parse_args()
@@ -138,6 +157,15 @@ def main():
 
     import numpy as np
     import torch
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        x = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        y = torch.empty_like(x)
+        for _ in range(10):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 10}))
+        return
     import synth
     import synth.device as sdev
     from paper_2606_29094_amd import dlm, engine
@@ -208,17 +236,20 @@ def main():
         F, B = work[dom]
         avg_s = prof[dom][1] / prof[dom][0] * 1e-3
         peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_F32_TFLOPS
+        traffic, traffic_src = measured_traffic(dom)
         ai = F / B
         if ai >= peak * 1e12 / (PEAK_HBM_GBS * 1e9):
             achieved = F / avg_s / 1e12
             roof = {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": peak,
-                    "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                    "unit": "TFLOP/s", "frac": achieved / peak, "traffic": traffic,
+                    "traffic_source": traffic_src, "algorithmic_bytes": B,
                     "flop_per_launch": F, "avg_launch_us": avg_s * 1e6}
         else:
             achieved = B / avg_s / 1e9
             roof = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
-                    "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
-                    "bytes_per_launch": B, "avg_launch_us": avg_s * 1e6}
+                    "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                    "traffic_source": traffic_src, "bytes_per_launch": B,
+                    "avg_launch_us": avg_s * 1e6}
     Fs, Bs = step_work(shape, L, L, m_avg)
     t_step = elapsed / args.steps
     step_roof = {"tflops": Fs / t_step / 1e12, "gbs": Bs / t_step / 1e9,

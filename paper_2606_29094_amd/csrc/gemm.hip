@@ -16,204 +16,10 @@
 // v_mfma_f32_16x16x32_bf16, fp32 uses v_mfma_f32_16x16x4_f32 (four per 16-byte
 // fragment, the k order is the same permutation for A and B).
 #include "common.h"
+#include "gemm_common.h"
 #include "kernels.h"
 
 namespace dlm {
-
-template <typename T> struct MfmaTraits;
-template <> struct MfmaTraits<bf16> {
-  static constexpr int kVec = 8;
-  __device__ __forceinline__ static f32x4 mma(const u32x4& a, const u32x4& b, f32x4 c) {
-    return mfma16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c);
-  }
-};
-template <> struct MfmaTraits<float> {
-  static constexpr int kVec = 4;
-  __device__ __forceinline__ static f32x4 mma(const u32x4& a, const u32x4& b, f32x4 c) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      c = mfma16_f32(__uint_as_float(a[j]), __uint_as_float(b[j]), c);
-    return c;
-  }
-};
-
-constexpr int kRowBytes = 128;          // k-tile bytes per row
-constexpr int kLdsRow = kRowBytes + 16; // padded LDS row stride
-
-// ------------------------------------------------------------ epilogues --
-// Each epilogue sees the wave's accumulators: acc[fm][fn][i] is the value at
-// row m0 + fm*16 + 4*(lane/16) + i, column n0 + fn*16 + lane%16.
-
-struct EpiStore {
-  float* C; int ldc; long split_stride; int M, N;
-  __device__ int b_row(int n) const { return n; }
-  template <int FM, int FN>
-  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
-    float* Cz = C + (long)blockIdx.z * split_stride;
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
-        if (m >= M) continue;
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          int n = n0 + fn * 16 + (lane & 15);
-          if (n < N) Cz[(long)m * ldc + n] = acc[fm][fn][i];
-        }
-      }
-  }
-};
-
-struct EpiScaledStore {
-  float* C; int ldc; int M, N; float scale;
-  __device__ int b_row(int n) const { return n; }
-  template <int FM, int FN>
-  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
-        if (m >= M) continue;
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          int n = n0 + fn * 16 + (lane & 15);
-          if (n < N) C[(long)m * ldc + n] = acc[fm][fn][i] * scale;
-        }
-      }
-  }
-};
-
-struct EpiAdd {
-  float* C; int ldc; int M, N;
-  __device__ int b_row(int n) const { return n; }
-  template <int FM, int FN>
-  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
-        if (m >= M) continue;
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          int n = n0 + fn * 16 + (lane & 15);
-          if (n < N) C[(long)m * ldc + n] += acc[fm][fn][i];
-        }
-      }
-  }
-};
-
-// Gate/up interleave: output column block of 32 = 16 gate columns followed by
-// the 16 up columns of the same ffn indices. GEMM column n maps to ffn index
-// f = (n / 32) * 16 + n % 16, gate when (n / 16) is even.
-template <typename T>
-struct EpiSwiGLU {
-  T* out; int ldo; int M; int F;   // F = d_ffn; GEMM N = 2F
-  __device__ int b_row(int n) const {
-    int f = (n >> 5) * 16 + (n & 15);
-    return ((n >> 4) & 1) ? F + f : f;
-  }
-  template <int FM, int FN>
-  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
-    static_assert(FN % 2 == 0, "gate/up pairs");
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
-        if (m >= M) continue;
-#pragma unroll
-        for (int fn = 0; fn < FN; fn += 2) {
-          int n = n0 + fn * 16;               // multiple of 32
-          int f = (n >> 5) * 16 + (lane & 15);
-          if (f >= F) continue;
-          float g = acc[fm][fn][i], u = acc[fm][fn + 1][i];
-          float s = g / (1.0f + __expf(-g));
-          out[(long)m * ldo + f] = from_f32<T>(s * u);
-        }
-      }
-  }
-};
-
-// Online softmax statistics of one row over a set of columns.
-struct RowStat { float m; float s; int i; };
-__device__ __forceinline__ RowStat combine(RowStat a, RowStat b) {
-  RowStat r;
-  r.m = fmaxf(a.m, b.m);
-  float sa = a.s == 0.f ? 0.f : a.s * __expf(a.m - r.m);
-  float sb = b.s == 0.f ? 0.f : b.s * __expf(b.m - r.m);
-  r.s = sa + sb;
-  r.i = a.m > b.m ? a.i : (b.m > a.m ? b.i : min(a.i, b.i));
-  return r;
-}
-
-// Fused LM head: per row and vocab tile, (max, sum exp(z - max), lowest argmax)
-// of z = acc * inv_tau; written to part_[m|s|i][tile][row].
-struct EpiLMHead {
-  float* pm; float* ps; int* pi; int M; int V; float inv_tau; int ld;  // ld = rows stride
-  __device__ int b_row(int n) const { return n; }
-  template <int FM, int FN>
-  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int wave_n,
-                             char* smem, int waves_n, int bm) const {
-    // stats per (fm, i) row for this lane over its FN columns
-    RowStat st[FM][4];
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        RowStat r = {-INFINITY, 0.f, 0x7fffffff};
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          int n = n0 + fn * 16 + (lane & 15);
-          if (n < V) {
-            float z = acc[fm][fn][i] * inv_tau;
-            RowStat c = {z, 1.f, n};
-            r = combine(r, c);
-          }
-        }
-        // across the 16 lanes that hold the other columns of these rows
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) {
-          RowStat x;
-          x.m = __shfl_xor(r.m, o, 64);
-          x.s = __shfl_xor(r.s, o, 64);
-          x.i = __shfl_xor(r.i, o, 64);
-          r = combine(r, x);
-        }
-        st[fm][i] = r;
-      }
-    // across the waves that share these rows (different column ranges): LDS
-    RowStat* buf = reinterpret_cast<RowStat*>(smem);
-    const int wave_m_row0 = m0 - blockIdx.y * bm;  // wave's row offset inside the block tile
-    __syncthreads();
-    if ((lane & 15) == 0) {
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          int r = wave_m_row0 + fm * 16 + 4 * (lane >> 4) + i;
-          buf[r * waves_n + wave_n] = st[fm][i];
-        }
-    }
-    __syncthreads();
-    const int tile = blockIdx.x;
-    for (int r = threadIdx.x; r < bm; r += blockDim.x) {
-      int m = blockIdx.y * bm + r;
-      if (m >= M) continue;
-      RowStat acc_r = buf[r * waves_n];
-      for (int w = 1; w < waves_n; ++w) acc_r = combine(acc_r, buf[r * waves_n + w]);
-      pm[(long)tile * ld + m] = acc_r.m;
-      ps[(long)tile * ld + m] = acc_r.s;
-      pi[(long)tile * ld + m] = acc_r.i;
-    }
-  }
-};
 
 // ---------------------------------------------------------------- kernel --
 template <typename T, int BM, int BN, int WAVES_M, int WAVES_N, class Epi>
@@ -320,9 +126,15 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(
 }
 
 // --------------------------------------------------------------- launch --
+template <class Epi>
+hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
+                          int K, int splits, const Epi& epi, hipStream_t st);
+int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads);
+
+// Register-staged kernel: any K that is a multiple of 16 bytes, fp32 or bf16.
 template <typename T, class Epi>
-static hipError_t launch(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
-                         int splits, const Epi& epi, hipStream_t st) {
+static hipError_t launch_rs(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
+                            int splits, const Epi& epi, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
   constexpr int BK = kRowBytes / sizeof(T);
   // split-K slices must tile K exactly: the consumers sum every slice
@@ -344,64 +156,114 @@ static hipError_t launch(const T* A, int lda, const T* B, int ldb, int M, int N,
   return hipGetLastError();
 }
 
-int gemm_split_count(int M, int N, int K, int num_cu) {
-  // enough blocks to cover the chip about twice; K slices stay >= 512
-  int bm = M <= 32 ? 32 : (M <= 64 ? 64 : 128);
-  long tiles = (long)ceil_div(N, 128) * ceil_div(M, bm);
-  int s = 1;
-  while (tiles * s < 2L * num_cu && K % (s * 2 * 64) == 0 && K / (s * 2) >= 512 && s < 16)
-    s *= 2;
-  return s;
+template <typename T, class Epi>
+static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
+                         int N, int K, const Epi& epi, hipStream_t st) {
+  if constexpr (sizeof(T) == 2) {
+    if (p.cfg >= 0) return gemm_dl_launch<Epi>(p.cfg, A, lda, B, ldb, M, N, K, p.splits, epi, st);
+  }
+  return launch_rs<T, Epi>(A, lda, B, ldb, M, N, K, p.splits, epi, st);
+}
+
+// Tile/split choice. bf16 with K a multiple of 64 uses the direct-load kernel.
+// A configuration runs `occ` blocks per CU at once; one such round over K =
+// 4096 takes t_round microseconds (fitted to launches whose weights stream
+// from HBM, MI355X). Estimate = rounds x t_round x (K slice / 4096), plus the
+// HBM traffic of the fp32 K slices when K is split (written by the GEMM, read
+// back by the consumer); the cheapest (configuration, split) wins.
+GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
+  GemmPlan best{-1, 1};
+  if (M <= 0 || N <= 0) return best;
+  if (es != 2 || K % 64 != 0) {
+    if (splittable) {
+      int bm = M <= 32 ? 32 : (M <= 64 ? 64 : 128);
+      long tiles = (long)ceil_div(N, 128) * ceil_div(M, bm);
+      int s = 1;
+      while (tiles * s < 2L * num_cu && K % (s * 2 * 64) == 0 && K / (s * 2) >= 512 && s < 8)
+        s *= 2;
+      best.splits = s;
+    }
+    return best;
+  }
+  struct Cand { int cfg; int occ; double t_round; int max_m; };
+  const Cand cands[] = {{6, 1, 124.0, 1 << 30}, {1, 2, 90.0, 1 << 30}, {10, 3, 75.0, 64}};
+  double best_t = 1e30;
+  for (const Cand& c : cands) {
+    if (M > c.max_m) continue;
+    int bm, bn, th;
+    gemm_dl_tile(c.cfg, &bm, &bn, &th);
+    for (int s = 1; s <= 8; s *= 2) {
+      if (s > 1 && (!splittable || (K / 64) % s != 0 || K / s < 512)) continue;
+      const long units = (long)ceil_div(M, bm) * ceil_div(N, bn) * s;
+      const long slots = (long)num_cu * c.occ;
+      const long rounds = (units + slots - 1) / slots;
+      double t = rounds * c.t_round * (double)(K / s) / 4096.0;
+      if (s > 1) t += (double)M * N * 4.0 * 2.0 * (s - 1) / 5.0e12 * 1e6;
+      if (t < best_t * 0.999) {
+        best_t = t;
+        best = GemmPlan{c.cfg, s};
+      }
+    }
+  }
+  return best;
 }
 
 template <typename T>
-hipError_t gemm_store_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
-                          int splits, float* C, int ldc, hipStream_t st) {
+hipError_t gemm_store_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
+                          int N, int K, float* C, int ldc, hipStream_t st) {
   EpiStore e{C, ldc, (long)M * ldc, M, N};
-  return launch<T>(A, lda, B, ldb, M, N, K, splits, e, st);
+  return launch<T>(p, A, lda, B, ldb, M, N, K, e, st);
 }
 
 template <typename T>
-hipError_t gemm_add_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
-                        float* C, int ldc, hipStream_t st) {
+hipError_t gemm_add_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M, int N,
+                        int K, float* C, int ldc, hipStream_t st) {
+  if (p.splits != 1) return hipErrorInvalidValue;
   EpiAdd e{C, ldc, M, N};
-  return launch<T>(A, lda, B, ldb, M, N, K, 1, e, st);
+  return launch<T>(p, A, lda, B, ldb, M, N, K, e, st);
 }
 
 template <typename T>
-hipError_t gemm_scaled_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
-                           float scale, float* C, int ldc, hipStream_t st) {
+hipError_t gemm_scaled_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
+                           int N, int K, float scale, float* C, int ldc, hipStream_t st) {
+  if (p.splits != 1) return hipErrorInvalidValue;
   EpiScaledStore e{C, ldc, M, N, scale};
-  return launch<T>(A, lda, B, ldb, M, N, K, 1, e, st);
+  return launch<T>(p, A, lda, B, ldb, M, N, K, e, st);
 }
 
 template <typename T>
-hipError_t gemm_swiglu(const T* A, int lda, const T* W, int ldw, int M, int F, int K,
-                       T* out, int ldo, hipStream_t st) {
+hipError_t gemm_swiglu(const GemmPlan& p, const T* A, int lda, const T* W, int ldw, int M, int F,
+                       int K, T* out, int ldo, hipStream_t st) {
+  if (p.splits != 1) return hipErrorInvalidValue;
   EpiSwiGLU<T> e{out, ldo, M, F};
-  return launch<T>(A, lda, W, ldw, M, 2 * F, K, 1, e, st);
+  return launch<T>(p, A, lda, W, ldw, M, 2 * F, K, e, st);
 }
 
-int lm_head_tiles(int V) { return ceil_div(V, 128); }
+int lm_head_tiles(const GemmPlan& p, int V) {
+  int bm = 128, bn = 128, th = 256;
+  if (p.cfg >= 0) gemm_dl_tile(p.cfg, &bm, &bn, &th);
+  return ceil_div(V, bn);
+}
 
 template <typename T>
-hipError_t gemm_lm_head(const T* U, int ldu, const T* W, int M, int V, int K, float inv_tau,
-                        float* pm, float* ps, int* pi, int ld, hipStream_t st) {
+hipError_t gemm_lm_head(const GemmPlan& p, const T* U, int ldu, const T* W, int M, int V, int K,
+                        float inv_tau, float* pm, float* ps, int* pi, int ld, hipStream_t st) {
+  if (p.splits != 1) return hipErrorInvalidValue;
   EpiLMHead e{pm, ps, pi, M, V, inv_tau, ld};
-  return launch<T>(U, ldu, W, K, M, V, K, 1, e, st);
+  return launch<T>(p, U, ldu, W, K, M, V, K, e, st);
 }
 
-#define INST(T)                                                                          \
-  template hipError_t gemm_store_f32<T>(const T*, int, const T*, int, int, int, int, int, \
-                                        float*, int, hipStream_t);                        \
-  template hipError_t gemm_add_f32<T>(const T*, int, const T*, int, int, int, int, float*, \
-                                      int, hipStream_t);                                  \
-  template hipError_t gemm_scaled_f32<T>(const T*, int, const T*, int, int, int, int,     \
-                                         float, float*, int, hipStream_t);                \
-  template hipError_t gemm_swiglu<T>(const T*, int, const T*, int, int, int, int, T*, int, \
-                                     hipStream_t);                                        \
-  template hipError_t gemm_lm_head<T>(const T*, int, const T*, int, int, int, float,      \
-                                      float*, float*, int*, int, hipStream_t);
+#define INST(T)                                                                                \
+  template hipError_t gemm_store_f32<T>(const GemmPlan&, const T*, int, const T*, int, int, int, \
+                                        int, float*, int, hipStream_t);                         \
+  template hipError_t gemm_add_f32<T>(const GemmPlan&, const T*, int, const T*, int, int, int,   \
+                                      int, float*, int, hipStream_t);                           \
+  template hipError_t gemm_scaled_f32<T>(const GemmPlan&, const T*, int, const T*, int, int,     \
+                                         int, int, float, float*, int, hipStream_t);            \
+  template hipError_t gemm_swiglu<T>(const GemmPlan&, const T*, int, const T*, int, int, int,    \
+                                     int, T*, int, hipStream_t);                                \
+  template hipError_t gemm_lm_head<T>(const GemmPlan&, const T*, int, const T*, int, int, int,   \
+                                      float, float*, float*, int*, int, hipStream_t);
 INST(bf16)
 INST(float)
 

@@ -1,0 +1,205 @@
+// Shared pieces of the GEMM kernels: MFMA operand traits and the tile
+// epilogues. Each epilogue sees a wave's accumulators: acc[fm][fn][i] is the
+// value at row m0 + fm*16 + 4*(lane/16) + i, column n0 + fn*16 + lane%16.
+#pragma once
+
+#include "common.h"
+
+namespace dlm {
+
+template <typename T> struct MfmaTraits;
+template <> struct MfmaTraits<bf16> {
+  static constexpr int kVec = 8;
+  __device__ __forceinline__ static f32x4 mma(const u32x4& a, const u32x4& b, f32x4 c) {
+    return mfma16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c);
+  }
+};
+template <> struct MfmaTraits<float> {
+  static constexpr int kVec = 4;
+  __device__ __forceinline__ static f32x4 mma(const u32x4& a, const u32x4& b, f32x4 c) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      c = mfma16_f32(__uint_as_float(a[j]), __uint_as_float(b[j]), c);
+    return c;
+  }
+};
+
+constexpr int kRowBytes = 128;          // k-tile bytes per row
+constexpr int kLdsRow = kRowBytes + 16; // padded LDS row stride
+
+// ------------------------------------------------------------ epilogues --
+// Each epilogue sees the wave's accumulators: acc[fm][fn][i] is the value at
+// row m0 + fm*16 + 4*(lane/16) + i, column n0 + fn*16 + lane%16.
+
+struct EpiStore {
+  float* C; int ldc; long split_stride; int M, N;
+  __device__ int b_row(int n) const { return n; }
+  template <int FM, int FN>
+  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
+                             char*, int, int) const {
+    float* Cz = C + (long)blockIdx.z * split_stride;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
+        if (m >= M) continue;
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          int n = n0 + fn * 16 + (lane & 15);
+          if (n < N) Cz[(long)m * ldc + n] = acc[fm][fn][i];
+        }
+      }
+  }
+};
+
+struct EpiScaledStore {
+  float* C; int ldc; int M, N; float scale;
+  __device__ int b_row(int n) const { return n; }
+  template <int FM, int FN>
+  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
+                             char*, int, int) const {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
+        if (m >= M) continue;
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          int n = n0 + fn * 16 + (lane & 15);
+          if (n < N) C[(long)m * ldc + n] = acc[fm][fn][i] * scale;
+        }
+      }
+  }
+};
+
+struct EpiAdd {
+  float* C; int ldc; int M, N;
+  __device__ int b_row(int n) const { return n; }
+  template <int FM, int FN>
+  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
+                             char*, int, int) const {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
+        if (m >= M) continue;
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          int n = n0 + fn * 16 + (lane & 15);
+          if (n < N) C[(long)m * ldc + n] += acc[fm][fn][i];
+        }
+      }
+  }
+};
+
+// Gate/up interleave: output column block of 32 = 16 gate columns followed by
+// the 16 up columns of the same ffn indices. GEMM column n maps to ffn index
+// f = (n / 32) * 16 + n % 16, gate when (n / 16) is even.
+template <typename T>
+struct EpiSwiGLU {
+  T* out; int ldo; int M; int F;   // F = d_ffn; GEMM N = 2F
+  __device__ int b_row(int n) const {
+    int f = (n >> 5) * 16 + (n & 15);
+    return ((n >> 4) & 1) ? F + f : f;
+  }
+  template <int FM, int FN>
+  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
+                             char*, int, int) const {
+    static_assert(FN % 2 == 0, "gate/up pairs");
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
+        if (m >= M) continue;
+#pragma unroll
+        for (int fn = 0; fn < FN; fn += 2) {
+          int n = n0 + fn * 16;               // multiple of 32
+          int f = (n >> 5) * 16 + (lane & 15);
+          if (f >= F) continue;
+          float g = acc[fm][fn][i], u = acc[fm][fn + 1][i];
+          float s = g / (1.0f + __expf(-g));
+          out[(long)m * ldo + f] = from_f32<T>(s * u);
+        }
+      }
+  }
+};
+
+// Online softmax statistics of one row over a set of columns.
+struct RowStat { float m; float s; int i; };
+__device__ __forceinline__ RowStat combine(RowStat a, RowStat b) {
+  RowStat r;
+  r.m = fmaxf(a.m, b.m);
+  float sa = a.s == 0.f ? 0.f : a.s * __expf(a.m - r.m);
+  float sb = b.s == 0.f ? 0.f : b.s * __expf(b.m - r.m);
+  r.s = sa + sb;
+  r.i = a.m > b.m ? a.i : (b.m > a.m ? b.i : min(a.i, b.i));
+  return r;
+}
+
+// Fused LM head: per row and vocab tile, (max, sum exp(z - max), lowest argmax)
+// of z = acc * inv_tau; written to part_[m|s|i][tile][row].
+struct EpiLMHead {
+  float* pm; float* ps; int* pi; int M; int V; float inv_tau; int ld;  // ld = rows stride
+  __device__ int b_row(int n) const { return n; }
+  template <int FM, int FN>
+  __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int wave_n,
+                             char* smem, int waves_n, int bm) const {
+    // stats per (fm, i) row for this lane over its FN columns
+    RowStat st[FM][4];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        RowStat r = {-INFINITY, 0.f, 0x7fffffff};
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          int n = n0 + fn * 16 + (lane & 15);
+          if (n < V) {
+            float z = acc[fm][fn][i] * inv_tau;
+            RowStat c = {z, 1.f, n};
+            r = combine(r, c);
+          }
+        }
+        // across the 16 lanes that hold the other columns of these rows
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          RowStat x;
+          x.m = __shfl_xor(r.m, o, 64);
+          x.s = __shfl_xor(r.s, o, 64);
+          x.i = __shfl_xor(r.i, o, 64);
+          r = combine(r, x);
+        }
+        st[fm][i] = r;
+      }
+    // across the waves that share these rows (different column ranges): LDS
+    RowStat* buf = reinterpret_cast<RowStat*>(smem);
+    const int wave_m_row0 = m0 - blockIdx.y * bm;  // wave's row offset inside the block tile
+    __syncthreads();
+    if ((lane & 15) == 0) {
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          int r = wave_m_row0 + fm * 16 + 4 * (lane >> 4) + i;
+          buf[r * waves_n + wave_n] = st[fm][i];
+        }
+    }
+    __syncthreads();
+    const int tile = blockIdx.x;
+    for (int r = threadIdx.x; r < bm; r += blockDim.x) {
+      int m = blockIdx.y * bm + r;
+      if (m >= M) continue;
+      RowStat acc_r = buf[r * waves_n];
+      for (int w = 1; w < waves_n; ++w) acc_r = combine(acc_r, buf[r * waves_n + w]);
+      pm[(long)tile * ld + m] = acc_r.m;
+      ps[(long)tile * ld + m] = acc_r.s;
+      pi[(long)tile * ld + m] = acc_r.i;
+    }
+  }
+};
+
+}  // namespace dlm

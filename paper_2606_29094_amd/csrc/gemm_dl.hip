@@ -1,0 +1,191 @@
+// bf16 NT GEMM with direct global->LDS loads (gfx950 global_load_lds_dwordx4).
+//
+// Each k-tile is 64 bf16 (128 bytes) of BM rows of A and BN rows of B. A wave
+// instruction moves 8 rows (1 KB): lane l writes LDS bytes [16 l, 16 l + 16)
+// of that kilobyte, and it fetches the global 16-byte chunk that belongs
+// there under an XOR swizzle (LDS chunk slot = global chunk ^ (row & 7)), so
+// that the 16 lanes that later read 16 consecutive rows of one chunk hit
+// distinct banks. Loads go STAGES-1 k-tiles ahead through a ring of LDS stages;
+// no registers hold tiles in flight. The MFMA part and the epilogues are the
+// same as the register-staged kernel.
+#include "common.h"
+#include "gemm_common.h"
+#include "kernels.h"
+
+namespace dlm {
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt in [3:0] and [15:14]; expcnt (7) and lgkmcnt (15) not waited on
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __attribute__((address_space(1))) const void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, class Epi>
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
+    int K, int k_per_split, Epi epi) {
+  constexpr int NW = WAVES_M * WAVES_N;
+  constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
+  constexpr int FM = TM / 16, FN = TN / 16;
+  constexpr int ROWS = BM + BN;
+  constexpr int STAGE = ROWS * 128;
+  constexpr int INSTR = ROWS / 8;
+  static_assert(INSTR % NW == 0, "rows per wave");
+  constexpr int PERW = INSTR / NW;
+  static_assert(STAGES >= 2 && (STAGES - 2) * PERW < 64, "stages");
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int kbeg = blockIdx.z * k_per_split;
+  const int kend = min(K, kbeg + k_per_split);
+  const int nkt = kend > kbeg ? (kend - kbeg) / 64 : 0;
+
+  // source of this lane for each of its wave's instructions (fixed over k)
+  const int cc = (lane & 7) ^ (lane >> 3);
+  const bf16* src[PERW];
+#pragma unroll
+  for (int j = 0; j < PERW; ++j) {
+    const int row = 8 * (wave * PERW + j) + (lane >> 3);
+    if (row < BM) {
+      const int m = min(m0 + row, M - 1);
+      src[j] = A + (long)m * lda + kbeg + cc * 8;
+    } else {
+      const int n = min(n0 + row - BM, N - 1);
+      src[j] = B + (long)epi.b_row(n) * ldb + kbeg + cc * 8;
+    }
+  }
+  auto issue = [&](int stage, int kt) {
+    char* dst = smem + stage * STAGE + wave * PERW * 1024;
+#pragma unroll
+    for (int j = 0; j < PERW; ++j)
+      __builtin_amdgcn_global_load_lds((gptr_t)(src[j] + kt * 64), (lptr_t)(dst + j * 1024), 16,
+                                       0, 0);
+  };
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int a = 0; a < FM; ++a)
+#pragma unroll
+    for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // fragment offsets: row R = base + (lane & 15), chunk c = 4 g + lane / 16,
+  // stored at slot c ^ (R & 7) = c ^ (lane & 7)
+  const int a_row = (wm * TM + (lane & 15)) * 128;
+  const int b_row = (BM + wn * TN + (lane & 15)) * 128;
+  const int c0 = ((0 * 4 + (lane >> 4)) ^ (lane & 7)) << 4;
+  const int c1 = ((1 * 4 + (lane >> 4)) ^ (lane & 7)) << 4;
+
+  auto compute = [&](int stage) {
+    const char* s = smem + stage * STAGE;
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const int co = g ? c1 : c0;
+      u32x4 af[FM], bfr[FN];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+        af[fm] = *reinterpret_cast<const u32x4*>(s + a_row + fm * 16 * 128 + co);
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        bfr[fn] = *reinterpret_cast<const u32x4*>(s + b_row + fn * 16 * 128 + co);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+          acc[fm][fn] = mfma16_bf16(__builtin_bit_cast(bf16x8, af[fm]),
+                                    __builtin_bit_cast(bf16x8, bfr[fn]), acc[fm][fn]);
+    }
+  };
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nkt) issue(s, s);
+
+  for (int kt = 0; kt < nkt; ++kt) {
+    // tiles kt+1 .. min(nkt-1, kt+STAGES-2) may stay in flight
+    const int ahead = min(STAGES - 2, nkt - 1 - kt);
+    if constexpr (STAGES == 2) {
+      wait_vmcnt<0>();
+    } else if constexpr (STAGES == 3) {
+      if (ahead >= 1) wait_vmcnt<PERW>(); else wait_vmcnt<0>();
+    } else {
+      static_assert(STAGES == 4, "2..4 stages");
+      if (ahead >= 2) wait_vmcnt<2 * PERW>();
+      else if (ahead == 1) wait_vmcnt<PERW>();
+      else wait_vmcnt<0>();
+    }
+    // Every wave has its own loads of tile kt in LDS and has finished reading
+    // the stage about to be refilled. A bare s_barrier: __syncthreads() would
+    // add a fence that drains every load in flight.
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + STAGES - 1 < nkt) issue((kt + STAGES - 1) % STAGES, kt + STAGES - 1);
+    compute(kt % STAGES);
+  }
+  __syncthreads();
+  epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM);
+}
+
+// Tile configurations (BM, BN, waves M x N, stages).
+#define DL_CONFIGS(X)       \
+  X(0, 128, 128, 2, 2, 3)   \
+  X(1, 128, 128, 2, 2, 2)   \
+  X(2, 128, 256, 2, 4, 3)   \
+  X(3, 256, 128, 4, 2, 3)   \
+  X(4, 64, 256, 1, 4, 3)    \
+  X(5, 32, 256, 1, 4, 4)    \
+  X(6, 256, 256, 2, 4, 2)   \
+  X(7, 128, 128, 2, 2, 4)   \
+  X(8, 256, 128, 4, 2, 2)   \
+  X(9, 128, 256, 2, 4, 2)   \
+  X(10, 64, 128, 2, 2, 2)
+
+int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
+  switch (cfg) {
+#define X(id, BM_, BN_, WM_, WN_, S_) \
+  case id: *bm = BM_; *bn = BN_; *threads = WM_ * WN_ * 64; return 1;
+    DL_CONFIGS(X)
+#undef X
+  }
+  return 0;
+}
+
+template <class Epi>
+hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
+                          int K, int splits, const Epi& epi, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K % 64 != 0 || splits < 1 || (K / 64) % splits != 0) return hipErrorInvalidValue;
+  const int kps = K / splits;
+  switch (cfg) {
+#define X(id, BM_, BN_, WM_, WN_, S_)                                                      \
+  case id: {                                                                             \
+    dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                  \
+    hipLaunchKernelGGL((gemm_dl_kernel<BM_, BN_, WM_, WN_, S_, Epi>), g, dim3(WM_ * WN_ * 64), \
+                       0, st, A, lda, B, ldb, M, N, K, kps, epi);                        \
+    return hipGetLastError();                                                            \
+  }
+    DL_CONFIGS(X)
+#undef X
+  }
+  return hipErrorInvalidValue;
+}
+
+template hipError_t gemm_dl_launch<EpiStore>(int, const bf16*, int, const bf16*, int, int, int,
+                                             int, int, const EpiStore&, hipStream_t);
+template hipError_t gemm_dl_launch<EpiAdd>(int, const bf16*, int, const bf16*, int, int, int,
+                                           int, int, const EpiAdd&, hipStream_t);
+template hipError_t gemm_dl_launch<EpiScaledStore>(int, const bf16*, int, const bf16*, int, int,
+                                                   int, int, int, const EpiScaledStore&,
+                                                   hipStream_t);
+template hipError_t gemm_dl_launch<EpiSwiGLU<bf16>>(int, const bf16*, int, const bf16*, int, int,
+                                                    int, int, int, const EpiSwiGLU<bf16>&,
+                                                    hipStream_t);
+template hipError_t gemm_dl_launch<EpiLMHead>(int, const bf16*, int, const bf16*, int, int, int,
+                                              int, int, const EpiLMHead&, hipStream_t);
+
+}  // namespace dlm

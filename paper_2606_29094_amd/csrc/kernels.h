@@ -44,24 +44,27 @@ __device__ __forceinline__ int plan_req_of_tile(const StepPlan& p, int tile) {
   return r;
 }
 
-// ---- GEMM family (gemm.hip) ----
-int gemm_split_count(int M, int N, int K, int num_cu);
+// ---- GEMM family (gemm.hip, gemm_dl.hip) ----
+// cfg >= 0: a direct-load tile configuration (bf16); cfg < 0: register-staged
+// kernel. splits: number of K slices (fp32 partial slices, summed by the consumer).
+struct GemmPlan { int cfg; int splits; };
+GemmPlan gemm_plan(int elem_bytes, int M, int N, int K, bool splittable, int num_cu);
 template <typename T>
-hipError_t gemm_store_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
-                          int splits, float* C, int ldc, hipStream_t st);
+hipError_t gemm_store_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
+                          int N, int K, float* C, int ldc, hipStream_t st);
 template <typename T>
-hipError_t gemm_add_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
-                        float* C, int ldc, hipStream_t st);
+hipError_t gemm_add_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M, int N,
+                        int K, float* C, int ldc, hipStream_t st);
 template <typename T>
-hipError_t gemm_scaled_f32(const T* A, int lda, const T* B, int ldb, int M, int N, int K,
-                           float scale, float* C, int ldc, hipStream_t st);
+hipError_t gemm_scaled_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
+                           int N, int K, float scale, float* C, int ldc, hipStream_t st);
 template <typename T>
-hipError_t gemm_swiglu(const T* A, int lda, const T* W, int ldw, int M, int F, int K,
-                       T* out, int ldo, hipStream_t st);
-int lm_head_tiles(int V);
+hipError_t gemm_swiglu(const GemmPlan& p, const T* A, int lda, const T* W, int ldw, int M, int F,
+                       int K, T* out, int ldo, hipStream_t st);
+int lm_head_tiles(const GemmPlan& p, int V);
 template <typename T>
-hipError_t gemm_lm_head(const T* U, int ldu, const T* W, int M, int V, int K, float inv_tau,
-                        float* pm, float* ps, int* pi, int ld, hipStream_t st);
+hipError_t gemm_lm_head(const GemmPlan& p, const T* U, int ldu, const T* W, int M, int V, int K,
+                        float inv_tau, float* pm, float* ps, int* pi, int ld, hipStream_t st);
 
 // ---- per-row kernels (rowwise.hip) ----
 template <typename T>
@@ -70,6 +73,10 @@ hipError_t embed_rows(const StepPlan& p, const T* E, int d, int vocab, int mask_
 template <typename T>
 hipError_t rmsnorm_rows(const float* h, const float* g, int n, int d, float eps, T* out,
                         hipStream_t st);
+// h[n] += sum of split-K slices (part may be null), then out = rmsnorm(h) (out may be null)
+template <typename T>
+hipError_t add_rmsnorm_rows(float* h, const float* part, int splits, long stride, const float* g,
+                            int n, int d, float eps, T* out, hipStream_t st);
 hipError_t rope_table(const StepPlan& p, int head_dim, float theta, float2* cs, hipStream_t st);
 template <typename T>
 hipError_t qkv_rope_scatter(const StepPlan& p, const float* qkv, int splits, long split_stride,

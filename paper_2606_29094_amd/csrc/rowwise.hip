@@ -49,22 +49,35 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
 }
 
 // out[n] = h[n] / sqrt(mean(h[n]^2) + eps) * g, fp32 math, stored as T.
+// With split-K slices (part != null), the row is first updated in place,
+// h[n] += sum_s part[s][n] (slices in order), so the residual update of the
+// previous projection and this norm take one pass over h. out may be null
+// (update only). rows/count select and bound the rows (final-norm gather).
 template <typename T>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h,
-                                                      const float* __restrict__ g, int d,
-                                                      float eps, T* __restrict__ out,
+__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ h,
+                                                      const float* __restrict__ part, int splits,
+                                                      long stride, const float* __restrict__ g,
+                                                      int d, float eps, T* __restrict__ out,
                                                       const int* __restrict__ rows,
                                                       const int* __restrict__ count) {
   __shared__ float red[4];
   const int i = blockIdx.x;
   if (count && i >= *count) return;
   const int src_row = rows ? rows[i] : i;
-  const float* x = h + (long)src_row * d;
+  float* x = h + (long)src_row * d;
   float ss = 0.f;
   for (int j = threadIdx.x * 4; j < d; j += 1024) {
     float4 v = *reinterpret_cast<const float4*>(x + j);
+    if (part) {
+      for (int s = 0; s < splits; ++s) {
+        const float4 p = *reinterpret_cast<const float4*>(part + s * stride + (long)src_row * d + j);
+        v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+      }
+      *reinterpret_cast<float4*>(x + j) = v;
+    }
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
+  if (!out) return;
   const float inv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)d + eps);
   T* o = out + (long)i * d;
   for (int j = threadIdx.x * 4; j < d; j += 1024) {
@@ -78,11 +91,21 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 }
 
 template <typename T>
+hipError_t add_rmsnorm_rows(float* h, const float* part, int splits, long stride, const float* g,
+                            int n, int d, float eps, T* out, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, h, part, splits, stride, g, d,
+                     eps, out, (const int*)nullptr, (const int*)nullptr);
+  return hipGetLastError();
+}
+
+template <typename T>
 hipError_t rmsnorm_rows(const float* h, const float* g, int n, int d, float eps, T* out,
                         hipStream_t st) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, h, g, d, eps, out,
-                     (const int*)nullptr, (const int*)nullptr);
+  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, const_cast<float*>(h),
+                     (const float*)nullptr, 0, 0L, g, d, eps, out, (const int*)nullptr,
+                     (const int*)nullptr);
   return hipGetLastError();
 }
 
@@ -91,8 +114,8 @@ hipError_t final_norm_gather(const float* h, const float* g, const int* lm_rows,
                              const int* lm_count, int m_max, int d, float eps, T* u,
                              hipStream_t st) {
   if (m_max == 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(m_max), dim3(256), 0, st, h, g, d, eps, u, lm_rows,
-                     lm_count);
+  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(m_max), dim3(256), 0, st, const_cast<float*>(h),
+                     (const float*)nullptr, 0, 0L, g, d, eps, u, lm_rows, lm_count);
   return hipGetLastError();
 }
 
@@ -139,23 +162,37 @@ __global__ __launch_bounds__(256) void qkv_rope_scatter_kernel(
   const int row_base = q.row0 + lrow0;
   const int pos_base = q.pos0 + lrow0;
 
-  auto load = [&](int n, int col) {
-    const float* src = qkv + (long)n * qkv_dim + col;
-    float v = src[0];
-    for (int s = 1; s < splits; ++s) v += src[(long)s * split_stride];
-    return v;
-  };
 
-  if (y < hq) {
-    for (int idx = threadIdx.x; idx < nvalid * HALF; idx += blockDim.x) {
-      const int rr = idx / HALF, i = idx % HALF;
+  // rotary pairs (i, i + HALF): each thread takes 4 consecutive i of one row
+  auto rotate = [&](int col0, T* dst_base, long dst_row_stride, bool kv) {
+    constexpr int QUADS = HALF / 4;
+    for (int idx = threadIdx.x; idx < nvalid * QUADS; idx += blockDim.x) {
+      const int rr = idx / QUADS, i = (idx % QUADS) * 4;
       const int n = row_base + rr;
-      const float x1 = load(n, y * DH + i), x2 = load(n, y * DH + i + HALF);
-      const float2 c = cs[(long)n * HALF + i];
-      T* o = q_out + (long)n * hq * DH + y * DH;
-      o[i] = from_f32<T>(x1 * c.x - x2 * c.y);
-      o[i + HALF] = from_f32<T>(x2 * c.x + x1 * c.y);
+      const float* src = qkv + (long)n * qkv_dim + col0 + i;
+      float4 a = *reinterpret_cast<const float4*>(src);
+      float4 b = *reinterpret_cast<const float4*>(src + HALF);
+      for (int sp = 1; sp < splits; ++sp) {
+        const float4 a2 = *reinterpret_cast<const float4*>(src + sp * split_stride);
+        const float4 b2 = *reinterpret_cast<const float4*>(src + sp * split_stride + HALF);
+        a.x += a2.x; a.y += a2.y; a.z += a2.z; a.w += a2.w;
+        b.x += b2.x; b.y += b2.y; b.z += b2.z; b.w += b2.w;
+      }
+      const float4 c01 = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i);
+      const float4 c23 = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i + 2);
+      T* o = dst_base + (kv ? (long)(pos_base + rr) : (long)n) * dst_row_stride;
+      o[i + 0] = from_f32<T>(a.x * c01.x - b.x * c01.y);
+      o[i + 1] = from_f32<T>(a.y * c01.z - b.y * c01.w);
+      o[i + 2] = from_f32<T>(a.z * c23.x - b.z * c23.y);
+      o[i + 3] = from_f32<T>(a.w * c23.z - b.w * c23.w);
+      o[i + HALF + 0] = from_f32<T>(b.x * c01.x + a.x * c01.y);
+      o[i + HALF + 1] = from_f32<T>(b.y * c01.z + a.y * c01.w);
+      o[i + HALF + 2] = from_f32<T>(b.z * c23.x + a.z * c23.y);
+      o[i + HALF + 3] = from_f32<T>(b.w * c23.z + a.w * c23.w);
     }
+  };
+  if (y < hq) {
+    rotate(y * DH, q_out + y * DH, (long)hq * DH, false);
     return;
   }
   const int j = y - hq;
@@ -163,18 +200,19 @@ __global__ __launch_bounds__(256) void qkv_rope_scatter_kernel(
   T* vb = vcache + ((long)(q.slot * hkv + j) * DH) * s_max;
   const int kcol = hq * DH + j * DH;
   const int vcol = (hq + hkv) * DH + j * DH;
-  for (int idx = threadIdx.x; idx < nvalid * HALF; idx += blockDim.x) {
-    const int rr = idx / HALF, i = idx % HALF;
-    const int n = row_base + rr;
-    const float x1 = load(n, kcol + i), x2 = load(n, kcol + i + HALF);
-    const float2 c = cs[(long)n * HALF + i];
-    T* o = kb + (long)(pos_base + rr) * DH;
-    o[i] = from_f32<T>(x1 * c.x - x2 * c.y);
-    o[i + HALF] = from_f32<T>(x2 * c.x + x1 * c.y);
-  }
-  for (int idx = threadIdx.x; idx < nvalid * DH; idx += blockDim.x) {
-    const int rr = idx / DH, d = idx % DH;
-    vt[d][rr] = from_f32<T>(load(row_base + rr, vcol + d));
+  rotate(kcol, kb, DH, true);
+  for (int idx = threadIdx.x; idx < nvalid * (DH / 4); idx += blockDim.x) {
+    const int rr = idx / (DH / 4), d = (idx % (DH / 4)) * 4;
+    const float* src = qkv + (long)(row_base + rr) * qkv_dim + vcol + d;
+    float4 v = *reinterpret_cast<const float4*>(src);
+    for (int sp = 1; sp < splits; ++sp) {
+      const float4 v2 = *reinterpret_cast<const float4*>(src + sp * split_stride);
+      v.x += v2.x; v.y += v2.y; v.z += v2.z; v.w += v2.w;
+    }
+    vt[d + 0][rr] = from_f32<T>(v.x);
+    vt[d + 1][rr] = from_f32<T>(v.y);
+    vt[d + 2][rr] = from_f32<T>(v.z);
+    vt[d + 3][rr] = from_f32<T>(v.w);
   }
   __syncthreads();
   for (int idx = threadIdx.x; idx < nvalid * DH; idx += blockDim.x) {
@@ -395,6 +433,8 @@ hipError_t unmask_select(const StepPlan& p, const float* conf, const int* tok,
                                     const uint8_t*, float*, hipStream_t);                      \
   template hipError_t rmsnorm_rows<T>(const float*, const float*, int, int, float, T*,         \
                                       hipStream_t);                                            \
+  template hipError_t add_rmsnorm_rows<T>(float*, const float*, int, long, const float*, int,  \
+                                          int, float, T*, hipStream_t);                        \
   template hipError_t final_norm_gather<T>(const float*, const float*, const int*, const int*, \
                                            int, int, float, T*, hipStream_t);                  \
   template hipError_t qkv_rope_scatter<T>(const StepPlan&, const float*, int, long,            \

@@ -122,23 +122,27 @@ namespace {
 struct Layout {
   size_t h, a, qkv, cs, q, ao, part, act, lm_rows, lm_count, req_off, req_cnt, u, pm, ps, pi,
       conf, tok, total;
+  GemmPlan g_qkv, g_o, g_gu, g_down, g_lm, g_logits;
   int s_qkv, s_o, s_down, tiles, m_max;
 };
-
-int splits_for(const dlm_model* m, int M, int N, int K) {
-  return gemm_split_count(M, N, K, m->num_cu);
-}
 
 Layout layout(const dlm_model* m, int n, int n_req) {
   const dlm_config& c = m->cfg;
   Layout L{};
   const int qkv_dim = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
   const int qd = c.n_q_heads * c.head_dim;
-  L.s_qkv = splits_for(m, n, qkv_dim, c.d_model);
-  L.s_o = splits_for(m, n, c.d_model, qd);
-  L.s_down = splits_for(m, n, c.d_model, c.d_ffn);
+  const int es_i = (int)m->es;
+  L.g_qkv = gemm_plan(es_i, n, qkv_dim, c.d_model, true, m->num_cu);
+  L.g_o = gemm_plan(es_i, n, c.d_model, qd, true, m->num_cu);
+  L.g_gu = gemm_plan(es_i, n, 2 * c.d_ffn, c.d_model, false, m->num_cu);
+  L.g_down = gemm_plan(es_i, n, c.d_model, c.d_ffn, true, m->num_cu);
   L.m_max = std::min(n, n_req * kMaxBlock);
-  L.tiles = lm_head_tiles(c.vocab);
+  L.g_lm = gemm_plan(es_i, L.m_max, c.vocab, c.d_model, false, m->num_cu);
+  L.g_logits = L.g_lm;
+  L.s_qkv = L.g_qkv.splits;
+  L.s_o = L.g_o.splits;
+  L.s_down = L.g_down.splits;
+  L.tiles = lm_head_tiles(L.g_lm, c.vocab);
   const size_t es = m->es;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -296,33 +300,41 @@ dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const Ste
   LAUNCH(m, st, "rope_table", rope_table(p, dh, cf.rope_theta, cs, st));
   LAUNCH(m, st, "embed", embed_rows<T>(p, reinterpret_cast<const T*>(m->embed), d, cf.vocab, cf.mask_id,
                          b->tokens, b->mask, h, st));
+  LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, m->layers[0].attn_norm, n, d, cf.rms_eps, a, st));
   for (int l = 0; l < cf.n_layers; ++l) {
     const dlm_layer_weights& w = m->layers[l];
     T* kc = reinterpret_cast<T*>(c->k_layer(l));
     T* vc = reinterpret_cast<T*>(c->v_layer(l));
-    LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, w.attn_norm, n, d, cf.rms_eps, a, st));
-    LAUNCH(m, st, "gemm_qkv", gemm_store_f32<T>(a, d, reinterpret_cast<const T*>(w.w_qkv), d, n, qkv_dim, d,
-                               L.s_qkv, qkv, qkv_dim, st));
+    LAUNCH(m, st, "gemm_qkv", gemm_store_f32<T>(L.g_qkv, a, d, reinterpret_cast<const T*>(w.w_qkv), d, n,
+                                                      qkv_dim, d, qkv, qkv_dim, st));
     LAUNCH(m, st, "rope_kv_write", qkv_rope_scatter<T>(p, qkv, L.s_qkv, (long)n * qkv_dim, cs, hq, hkv, dh, q, kc, vc,
                                  c->s_max, st));
     LAUNCH(m, st, "attention", attention<T>(p, q, kc, vc, c->s_max, hq, hkv, dh, ao, st));
+    // O projection; its residual update is fused into the FFN norm when K is split
     if (L.s_o == 1) {
-      LAUNCH(m, st, "gemm_o", gemm_add_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, h, d, st));
+      LAUNCH(m, st, "gemm_o", gemm_add_f32<T>(L.g_o, ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d,
+                                                  qd, h, d, st));
+      LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, w.ffn_norm, n, d, cf.rms_eps, a, st));
     } else {
-      LAUNCH(m, st, "gemm_o", gemm_store_f32<T>(ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d, qd, L.s_o,
-                                 part, d, st));
-      LAUNCH(m, st, "splitk_reduce", add_partials(part, L.s_o, (long)n * d, n, d, h, st));
+      LAUNCH(m, st, "gemm_o", gemm_store_f32<T>(L.g_o, ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d,
+                                                    qd, part, d, st));
+      LAUNCH(m, st, "residual_rmsnorm", add_rmsnorm_rows<T>(h, part, L.s_o, (long)n * d, w.ffn_norm, n, d,
+                                                                cf.rms_eps, a, st));
     }
-    LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, w.ffn_norm, n, d, cf.rms_eps, a, st));
-    LAUNCH(m, st, "gemm_gate_up_swiglu", gemm_swiglu<T>(a, d, reinterpret_cast<const T*>(w.w_gate_up), d, n, cf.d_ffn, d, act,
+    LAUNCH(m, st, "gemm_gate_up_swiglu", gemm_swiglu<T>(L.g_gu, a, d, reinterpret_cast<const T*>(w.w_gate_up), d, n, cf.d_ffn, d, act,
                             cf.d_ffn, st));
+    // down projection; its residual update is fused into the next layer's norm
+    const float* next_norm = l + 1 < cf.n_layers ? m->layers[l + 1].attn_norm : nullptr;
+    T* next_a = l + 1 < cf.n_layers ? a : nullptr;
     if (L.s_down == 1) {
-      LAUNCH(m, st, "gemm_down", gemm_add_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n, d,
+      LAUNCH(m, st, "gemm_down", gemm_add_f32<T>(L.g_down, act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n, d,
                                cf.d_ffn, h, d, st));
+      if (next_a) LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, next_norm, n, d, cf.rms_eps, a, st));
     } else {
-      LAUNCH(m, st, "gemm_down", gemm_store_f32<T>(act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down), cf.d_ffn, n,
-                                 d, cf.d_ffn, L.s_down, part, d, st));
-      LAUNCH(m, st, "splitk_reduce", add_partials(part, L.s_down, (long)n * d, n, d, h, st));
+      LAUNCH(m, st, "gemm_down", gemm_store_f32<T>(L.g_down, act, cf.d_ffn, reinterpret_cast<const T*>(w.w_down),
+                                                       cf.d_ffn, n, d, cf.d_ffn, part, d, st));
+      LAUNCH(m, st, "residual_rmsnorm", add_rmsnorm_rows<T>(h, part, L.s_down, (long)n * d, next_norm, n, d,
+                                                                cf.rms_eps, next_a, st));
     }
   }
   return DLM_OK;
@@ -347,7 +359,7 @@ dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPl
                           req_cnt, st));
   LAUNCH(m, st, "final_norm", final_norm_gather<T>(h, m->final_norm, lm_rows, lm_count, m_max, d, cf.rms_eps, u, st));
   if (tail == Tail::Logits) {
-    LAUNCH(m, st, "gemm_logits", gemm_scaled_f32<T>(u, d, reinterpret_cast<const T*>(m->lm_head), d, m_max, cf.vocab,
+    LAUNCH(m, st, "gemm_logits", gemm_scaled_f32<T>(L.g_logits, u, d, reinterpret_cast<const T*>(m->lm_head), d, m_max, cf.vocab,
                                 d, cf.inv_tau, logits, cf.vocab, st));
     return DLM_OK;
   }
@@ -356,7 +368,7 @@ dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPl
   int* pi = reinterpret_cast<int*>(ws + L.pi);
   float* conf = reinterpret_cast<float*>(ws + L.conf);
   int* tok = reinterpret_cast<int*>(ws + L.tok);
-  LAUNCH(m, st, "lm_head", gemm_lm_head<T>(u, d, reinterpret_cast<const T*>(m->lm_head), m_max, cf.vocab, d,
+  LAUNCH(m, st, "lm_head", gemm_lm_head<T>(L.g_lm, u, d, reinterpret_cast<const T*>(m->lm_head), m_max, cf.vocab, d,
                            cf.inv_tau, pm, ps, pi, L.m_max, st));
   LAUNCH(m, st, "lm_combine", lm_combine(pm, ps, pi, L.tiles, L.m_max, lm_count, m_max, conf, tok, st));
   LAUNCH(m, st, "unmask", unmask_select(p, conf, tok, req_off, b->tokens, b->mask, out->n_unmasked, out->pos,
@@ -593,7 +605,8 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
   if (!workspace) return fail(DLM_EINVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
     return fail(DLM_EINVAL, "workspace is not 256-byte aligned");
-  const int tiles = lm_head_tiles(m->cfg.vocab);
+  const GemmPlan gp = gemm_plan((int)m->es, m_rows, m->cfg.vocab, m->cfg.d_model, false, m->num_cu);
+  const int tiles = lm_head_tiles(gp, m->cfg.vocab);
   const size_t stat = align_up((size_t)tiles * m_rows * 4, 256);
   const size_t need = 3 * stat + 256;
   if (ws_bytes < need) return fail(DLM_ESIZE, "workspace of %zu bytes; needs %zu", ws_bytes, need);
@@ -607,11 +620,11 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
   HIPCHECK(hipGetLastError());
   const dlm_config& cf = m->cfg;
   if (cf.dtype == DLM_BF16) {
-    HIPCHECK(gemm_lm_head<bf16>(reinterpret_cast<const bf16*>(u_rows), cf.d_model,
+    HIPCHECK(gemm_lm_head<bf16>(gp, reinterpret_cast<const bf16*>(u_rows), cf.d_model,
                                 reinterpret_cast<const bf16*>(m->lm_head), m_rows, cf.vocab,
                                 cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, st));
   } else {
-    HIPCHECK(gemm_lm_head<float>(reinterpret_cast<const float*>(u_rows), cf.d_model,
+    HIPCHECK(gemm_lm_head<float>(gp, reinterpret_cast<const float*>(u_rows), cf.d_model,
                                  reinterpret_cast<const float*>(m->lm_head), m_rows, cf.vocab,
                                  cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, st));
   }
