@@ -36,7 +36,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* 
   __shared__ __attribute__((aligned(16))) bf16 ks[kKeyTile * KS];
   __shared__ __attribute__((aligned(16))) bf16 vs[DH * VS];
 
-  const int tile = blockIdx.x, h = blockIdx.y;
+  // head-major grid: consecutive blocks (which the dispatcher spreads over the
+  // XCDs round-robin) are different heads, so the query tiles of one head
+  // (same K/V) land on the same XCD and share its L2
+  const int h = blockIdx.x, tile = blockIdx.y;
   const int r = plan_req_of_tile(p, tile);
   const ReqPlan& rq = p.r[r];
   const int lrow0 = (tile - rq.tile0) * kQTile;
@@ -67,34 +70,56 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* 
   for (int i = 0; i < NDB; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int ntiles = ceil_div(L, kKeyTile);
-  for (int t = 0; t < ntiles; ++t) {
-    const int key0 = t * kKeyTile;
-    __syncthreads();   // previous tile fully consumed
-    // K tile: 64 keys x DH, 16-byte chunks
-    for (int c = tid; c < kKeyTile * (DH / 8); c += 256) {
+  // K/V^T tiles go through registers: the next tile's global loads are issued
+  // before the current tile's MFMAs and written to LDS after them.
+  constexpr int KCH = kKeyTile * (DH / 8) / 256;   // 16-byte K chunks per thread
+  constexpr int VCH = DH * (kKeyTile / 8) / 256;   // 16-byte V^T chunks per thread
+  u32x4 kreg[KCH], vreg[VCH];
+  auto load_tile = [&](int key0) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * 256;
       const int kk = c / (DH / 8), cc = c % (DH / 8);
-      u32x4 v = u32x4{0u, 0u, 0u, 0u};
-      if (key0 + kk < L) v = *reinterpret_cast<const u32x4*>(kb + (long)(key0 + kk) * DH + cc * 8);
-      *reinterpret_cast<u32x4*>(ks + kk * KS + cc * 8) = v;
+      kreg[i] = key0 + kk < L
+                    ? *reinterpret_cast<const u32x4*>(kb + (long)(key0 + kk) * DH + cc * 8)
+                    : u32x4{0u, 0u, 0u, 0u};
     }
-    // V^T tile: DH rows x 64 keys
-    for (int c = tid; c < DH * (kKeyTile / 8); c += 256) {
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = tid + i * 256;
       const int d = c / (kKeyTile / 8), cc = c % (kKeyTile / 8);
       const int kk0 = key0 + cc * 8;
       const bf16* src = vb + (long)d * s_max + kk0;
-      u32x4 v;
       if (kk0 + 8 <= L) {
-        v = *reinterpret_cast<const u32x4*>(src);
+        vreg[i] = *reinterpret_cast<const u32x4*>(src);
       } else {
         bf16 tmp[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) tmp[e] = (kk0 + e < L) ? src[e] : (bf16)0.0f;
-        v = *reinterpret_cast<const u32x4*>(tmp);
+        vreg[i] = *reinterpret_cast<const u32x4*>(tmp);
       }
-      *reinterpret_cast<u32x4*>(vs + d * VS + cc * 8) = v;
     }
-    __syncthreads();
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * 256;
+      *reinterpret_cast<u32x4*>(ks + (c / (DH / 8)) * KS + (c % (DH / 8)) * 8) = kreg[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int c = tid + i * 256;
+      *reinterpret_cast<u32x4*>(vs + (c / (kKeyTile / 8)) * VS + (c % (kKeyTile / 8)) * 8) = vreg[i];
+    }
+  };
+
+  const int ntiles = ceil_div(L, kKeyTile);
+  load_tile(0);
+  store_tile();
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int key0 = t * kKeyTile;
+    if (t + 1 < ntiles) load_tile(key0 + kKeyTile);
 
     // S^T blocks: sblk[kb][i] = score(key = 16*kb + 4*g + i, query = lane&15)
     f32x4 sblk[4];
@@ -159,6 +184,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* 
         o[db] = mfma16_bf16(a, ph, o[db]);
         o[db] = mfma16_bf16(a, pl, o[db]);
       }
+    }
+    if (t + 1 < ntiles) {
+      __syncthreads();   // every wave is done with tile t
+      store_tile();
+      __syncthreads();
     }
   }
   // finish: l over the 4 lanes sharing the query, normalise, store
@@ -244,7 +274,7 @@ hipError_t attention<bf16>(const StepPlan& p, const bf16* q, const bf16* kc, con
                            int s_max, int hq, int hkv, int dh, bf16* out, hipStream_t st) {
   if (p.n_tiles == 0) return hipSuccess;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
-  dim3 g(p.n_tiles, hq);
+  dim3 g(hq, p.n_tiles);
   if (dh == 128)
     hipLaunchKernelGGL(attn_bf16_kernel<128>, g, dim3(256), 0, st, p, q, kc, vc, s_max, hq, hkv,
                        out, scale_log2);

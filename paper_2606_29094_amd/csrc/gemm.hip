@@ -15,6 +15,8 @@
 // vectors, prefetched into registers one k-tile ahead. bf16 uses
 // v_mfma_f32_16x16x32_bf16, fp32 uses v_mfma_f32_16x16x4_f32 (four per 16-byte
 // fragment, the k order is the same permutation for A and B).
+#include <algorithm>
+
 #include "common.h"
 #include "gemm_common.h"
 #include "kernels.h"
@@ -166,11 +168,13 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 }
 
 // Tile/split choice. bf16 with K a multiple of 64 uses the direct-load kernel.
-// A configuration runs `occ` blocks per CU at once; one such round over K =
-// 4096 takes t_round microseconds (fitted to launches whose weights stream
-// from HBM, MI355X). Estimate = rounds x t_round x (K slice / 4096), plus the
-// HBM traffic of the fp32 K slices when K is split (written by the GEMM, read
-// back by the consumer); the cheapest (configuration, split) wins.
+// A configuration keeps `occ` blocks per CU resident; a full round of them
+// over K = 4096 takes t_round microseconds (fitted to launches whose weights
+// stream from HBM, MI355X). A last, partly filled round of a multi-block
+// configuration costs max(0.7, fill) of a full one (a lone 4-wave block on a
+// CU is latency-bound). Estimate = rounds x t_round x (K slice / 4096), plus
+// the HBM traffic of the fp32 K slices when K is split (written by the GEMM,
+// read back by the consumer); the cheapest (configuration, split) wins.
 GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
   GemmPlan best{-1, 1};
   if (M <= 0 || N <= 0) return best;
@@ -185,18 +189,25 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
     }
     return best;
   }
-  struct Cand { int cfg; int occ; double t_round; int max_m; };
-  const Cand cands[] = {{6, 1, 124.0, 1 << 30}, {1, 2, 90.0, 1 << 30}, {10, 3, 75.0, 64}};
+  // 128x192 (cfg 22) is used only without K splits: measured slower than
+  // 128x128 on the N = 4096 projections it would otherwise win in the model.
+  struct Cand { int cfg; int occ; double t_round; int max_m; bool unsplit_only; };
+  const Cand cands[] = {{21, 1, 105.0, 1 << 30, false}, {22, 2, 100.0, 1 << 30, true},
+                        {6, 1, 124.0, 1 << 30, false}, {1, 2, 90.0, 1 << 30, false},
+                        {10, 3, 75.0, 64, false}};
   double best_t = 1e30;
   for (const Cand& c : cands) {
-    if (M > c.max_m) continue;
+    if (M > c.max_m || (c.unsplit_only && splittable)) continue;
     int bm, bn, th;
     gemm_dl_tile(c.cfg, &bm, &bn, &th);
     for (int s = 1; s <= 8; s *= 2) {
       if (s > 1 && (!splittable || (K / 64) % s != 0 || K / s < 512)) continue;
       const long units = (long)ceil_div(M, bm) * ceil_div(N, bn) * s;
       const long slots = (long)num_cu * c.occ;
-      const long rounds = (units + slots - 1) / slots;
+      const long full = units / slots;
+      const double fill = (double)(units - full * slots) / slots;
+      double rounds = (double)full;
+      if (fill > 0) rounds += c.occ > 1 ? std::max(0.7, fill) : 1.0;
       double t = rounds * c.t_round * (double)(K / s) / 4096.0;
       if (s > 1) t += (double)M * N * 4.0 * 2.0 * (s - 1) / 5.0e12 * 1e6;
       if (t < best_t * 0.999) {

@@ -24,16 +24,21 @@ __device__ __forceinline__ void wait_vmcnt() {
 typedef __attribute__((address_space(1))) const void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, class Epi>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int RB, class Epi>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int k_per_split, Epi epi) {
+  static_assert(RB == 64 || RB == 128, "k-tile row bytes");
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   constexpr int FM = TM / 16, FN = TN / 16;
+  constexpr int BK = RB / 2;              // bf16 per row per k-tile
+  constexpr int CPR = RB / 16;            // 16-byte chunks per row
+  constexpr int RPI = 1024 / RB;          // rows per 1 KB wave instruction
+  constexpr int KG = RB / 64;             // 32-wide k groups per k-tile
   constexpr int ROWS = BM + BN;
-  constexpr int STAGE = ROWS * 128;
-  constexpr int INSTR = ROWS / 8;
+  constexpr int STAGE = ROWS * RB;
+  constexpr int INSTR = ROWS / RPI;
   static_assert(INSTR % NW == 0, "rows per wave");
   constexpr int PERW = INSTR / NW;
   static_assert(STAGES >= 2 && (STAGES - 2) * PERW < 64, "stages");
@@ -44,14 +49,17 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int kbeg = blockIdx.z * k_per_split;
   const int kend = min(K, kbeg + k_per_split);
-  const int nkt = kend > kbeg ? (kend - kbeg) / 64 : 0;
+  const int nkt = kend > kbeg ? (kend - kbeg) / BK : 0;
 
+  // LDS chunk slot of global chunk c in row r: c ^ swz(r); 8 consecutive rows
+  // (two per 128-byte bank line for 64-byte rows) map to distinct banks.
+  auto swz = [](int r) { return CPR == 8 ? (r & 7) : ((r >> 1) & 3); };
   // source of this lane for each of its wave's instructions (fixed over k)
-  const int cc = (lane & 7) ^ (lane >> 3);
   const bf16* src[PERW];
 #pragma unroll
   for (int j = 0; j < PERW; ++j) {
-    const int row = 8 * (wave * PERW + j) + (lane >> 3);
+    const int row = RPI * (wave * PERW + j) + lane / CPR;
+    const int cc = (lane % CPR) ^ swz(row);
     if (row < BM) {
       const int m = min(m0 + row, M - 1);
       src[j] = A + (long)m * lda + kbeg + cc * 8;
@@ -64,7 +72,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     char* dst = smem + stage * STAGE + wave * PERW * 1024;
 #pragma unroll
     for (int j = 0; j < PERW; ++j)
-      __builtin_amdgcn_global_load_lds((gptr_t)(src[j] + kt * 64), (lptr_t)(dst + j * 1024), 16,
+      __builtin_amdgcn_global_load_lds((gptr_t)(src[j] + kt * BK), (lptr_t)(dst + j * 1024), 16,
                                        0, 0);
   };
 
@@ -74,25 +82,25 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
 #pragma unroll
     for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // fragment offsets: row R = base + (lane & 15), chunk c = 4 g + lane / 16,
-  // stored at slot c ^ (R & 7) = c ^ (lane & 7)
-  const int a_row = (wm * TM + (lane & 15)) * 128;
-  const int b_row = (BM + wn * TN + (lane & 15)) * 128;
-  const int c0 = ((0 * 4 + (lane >> 4)) ^ (lane & 7)) << 4;
-  const int c1 = ((1 * 4 + (lane >> 4)) ^ (lane & 7)) << 4;
+  // fragment offsets: row R = base + (lane & 15) with base a multiple of 16,
+  // chunk c = 4 g + lane / 16, stored at slot c ^ swz(R) = c ^ swz(lane & 15)
+  const int a_row = (wm * TM + (lane & 15)) * RB;
+  const int b_row = (BM + wn * TN + (lane & 15)) * RB;
+  int co[KG];
+#pragma unroll
+  for (int g = 0; g < KG; ++g) co[g] = ((g * 4 + (lane >> 4)) ^ swz(lane & 15)) << 4;
 
   auto compute = [&](int stage) {
     const char* s = smem + stage * STAGE;
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      const int co = g ? c1 : c0;
+    for (int g = 0; g < KG; ++g) {
       u32x4 af[FM], bfr[FN];
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
-        af[fm] = *reinterpret_cast<const u32x4*>(s + a_row + fm * 16 * 128 + co);
+        af[fm] = *reinterpret_cast<const u32x4*>(s + a_row + fm * 16 * RB + co[g]);
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn)
-        bfr[fn] = *reinterpret_cast<const u32x4*>(s + b_row + fn * 16 * 128 + co);
+        bfr[fn] = *reinterpret_cast<const u32x4*>(s + b_row + fn * 16 * RB + co[g]);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -113,9 +121,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
       wait_vmcnt<0>();
     } else if constexpr (STAGES == 3) {
       if (ahead >= 1) wait_vmcnt<PERW>(); else wait_vmcnt<0>();
-    } else {
-      static_assert(STAGES == 4, "2..4 stages");
+    } else if constexpr (STAGES == 4) {
       if (ahead >= 2) wait_vmcnt<2 * PERW>();
+      else if (ahead == 1) wait_vmcnt<PERW>();
+      else wait_vmcnt<0>();
+    } else {
+      static_assert(STAGES == 5, "2..5 stages");
+      if (ahead >= 3) wait_vmcnt<3 * PERW>();
+      else if (ahead == 2) wait_vmcnt<2 * PERW>();
       else if (ahead == 1) wait_vmcnt<PERW>();
       else wait_vmcnt<0>();
     }
@@ -131,23 +144,25 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM);
 }
 
-// Tile configurations (BM, BN, waves M x N, stages).
-#define DL_CONFIGS(X)       \
-  X(0, 128, 128, 2, 2, 3)   \
-  X(1, 128, 128, 2, 2, 2)   \
-  X(2, 128, 256, 2, 4, 3)   \
-  X(3, 256, 128, 4, 2, 3)   \
-  X(4, 64, 256, 1, 4, 3)    \
-  X(5, 32, 256, 1, 4, 4)    \
-  X(6, 256, 256, 2, 4, 2)   \
-  X(7, 128, 128, 2, 2, 4)   \
-  X(8, 256, 128, 4, 2, 2)   \
-  X(9, 128, 256, 2, 4, 2)   \
-  X(10, 64, 128, 2, 2, 2)
+// Tile configurations (BM, BN, waves M x N, stages, k-tile row bytes).
+#define DL_CONFIGS(X)            \
+  X(1, 128, 128, 2, 2, 2, 128)   \
+  X(6, 256, 256, 2, 4, 2, 128)   \
+  X(10, 64, 128, 2, 2, 2, 128)   \
+  X(14, 256, 256, 2, 4, 4, 64)   \
+  X(15, 256, 256, 2, 4, 3, 64)   \
+  X(16, 128, 128, 2, 2, 4, 64)   \
+  X(17, 128, 128, 2, 2, 3, 64)   \
+  X(18, 128, 256, 2, 4, 4, 64)   \
+  X(19, 256, 128, 4, 2, 4, 64)   \
+  X(20, 64, 128, 2, 2, 4, 64)    \
+  X(21, 256, 192, 4, 2, 2, 128)  \
+  X(22, 128, 192, 2, 2, 2, 128)  \
+  X(23, 256, 192, 2, 2, 2, 128)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, S_) \
+#define X(id, BM_, BN_, WM_, WN_, S_, RB_) \
   case id: *bm = BM_; *bn = BN_; *threads = WM_ * WN_ * 64; return 1;
     DL_CONFIGS(X)
 #undef X
@@ -162,10 +177,11 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
   if (K % 64 != 0 || splits < 1 || (K / 64) % splits != 0) return hipErrorInvalidValue;
   const int kps = K / splits;
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, S_)                                                      \
+#define X(id, BM_, BN_, WM_, WN_, S_, RB_)                                                 \
   case id: {                                                                             \
     dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                  \
-    hipLaunchKernelGGL((gemm_dl_kernel<BM_, BN_, WM_, WN_, S_, Epi>), g, dim3(WM_ * WN_ * 64), \
+    hipLaunchKernelGGL((gemm_dl_kernel<BM_, BN_, WM_, WN_, S_, RB_, Epi>), g,             \
+                       dim3(WM_ * WN_ * 64),                                             \
                        0, st, A, lda, B, ldb, M, N, K, kps, epi);                        \
     return hipGetLastError();                                                            \
   }
