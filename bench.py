@@ -1,18 +1,22 @@
 #!/usr/bin/env python3
 """Denoising-step throughput on one MI355X.
 
-Workload (default): the bf16 MHA model shaped like LLaDA-8B (32 layers, d 4096,
+Default workload: the bf16 MHA model shaped like LLaDA-8B (32 layers, d 4096,
 32 heads of 128, SwiGLU 12288, vocab 126464; synthetic N(0, 0.02) weights),
 batch 1, 256 random prompt tokens + 256 [MASK] tokens decoded in blocks of 32,
 no cache (every step recomputes all 512 positions), threshold 0.9, logits
 scaled by the calibrated 1/tau. One step = one dlm_denoise_step call (the whole
-hot path: embedding, 32 layers, fused LM head and confidence, unmask) plus the
-per-step readback of the unmask count. When the generation finishes the
-request is re-admitted with its prompt and the timing continues.
+hot path: embedding, every layer, fused LM head and confidence, unmask) plus
+the per-step read-back of the unmask counts. A finished request is replaced at
+once (the same prompt again, or the slot's next request for the heterogeneous
+workload), so the batch stays full.
+
+--workload selects the other configurations (batch 8 with prefix or dual
+cache, the heterogeneous batch of 32, the GQA batch of 64).
 
 Prints one JSON line: steps/s (value), unmasked tokens/s, the roofline of the
-dominant kernel (HIP events on the launch stream over the timed region), the
-whole-step roofline, and the CPU oracle timed on a bounded sample.
+dominant kernel (in-library HIP events on the launch stream over the timed
+region), the whole-step roofline, and the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -28,12 +32,12 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+GOLDEN = {"mha-8b": "mha_8b_step1.json", "gqa-7b": "gqa_7b_step1.json",
+          "tiny-fp32": "tiny_fp32.json"}
 
 
 def load_inv_tau(model_name: str):
-    path = os.path.join(ROOT, "tests", "golden",
-                        {"mha-8b": "mha_8b_step1.json", "gqa-7b": "gqa_7b_step1.json",
-                         "tiny-fp32": "tiny_fp32.json"}[model_name])
+    path = os.path.join(ROOT, "tests", "golden", GOLDEN[model_name])
     with open(path) as f:
         return float(json.load(f)["inv_tau"]), os.path.relpath(path, ROOT)
 
@@ -54,45 +58,62 @@ def measured_traffic(kernel_class: str):
     return float(t["hbm_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
 
-def kernel_work(shape, n_rows, seq_len, m_rows):
-    """Algorithmic FLOPs and HBM bytes of one launch of each kernel class for a
-    single-request no-cache step (n_rows recomputed rows, keys = seq_len,
-    m_rows LM-head rows)."""
-    d, dh, hq, hkv, ffn, V = (shape.d_model, shape.head_dim, shape.n_q_heads,
-                              shape.n_kv_heads, shape.d_ffn, shape.vocab)
+def step_rows(reqs, mode):
+    """(recomputed rows, keys) of each request for the step about to run."""
+    out = []
+    for r in reqs:
+        s = r.block_start
+        if mode == "none" or r.refreshed_block != s:
+            out.append((r.seq_len, r.seq_len))
+        elif mode == "dual":
+            out.append((r.block_len, r.seq_len))
+        else:
+            out.append((r.seq_len - s, r.seq_len))
+    return out
+
+
+def class_work(shape, rows, m_rows):
+    """Algorithmic FLOPs and HBM bytes of each kernel class in one step
+    (all layers), given per-request (recomputed rows, keys) and LM-head rows."""
+    d, dh, hq, hkv, ffn, V, nl = (shape.d_model, shape.head_dim, shape.n_q_heads,
+                                  shape.n_kv_heads, shape.d_ffn, shape.vocab, shape.n_layers)
     es = 2 if shape.dtype == "bf16" else 4
     qkv = (hq + 2 * hkv) * dh
     qd = hq * dh
-    N = n_rows
-    w = {
-        "gemm_qkv": (2.0 * N * d * qkv, es * (qkv * d + N * d) + 4 * N * qkv),
-        "gemm_o": (2.0 * N * qd * d, es * (d * qd + N * qd) + 8 * N * d),
-        "gemm_gate_up_swiglu": (2.0 * N * d * 2 * ffn, es * (2 * ffn * d + N * d + N * ffn)),
-        "gemm_down": (2.0 * N * ffn * d, es * (d * ffn + N * ffn) + 8 * N * d),
-        "attention": (4.0 * N * seq_len * hq * dh, es * (2 * N * qd + 2 * seq_len * hkv * dh)),
+    N = sum(n for n, _ in rows)
+    qk = sum(n * L for n, L in rows)
+    keys = sum(L for _, L in rows)
+    return {
+        "gemm_qkv": (nl * 2.0 * N * d * qkv, nl * (es * (qkv * d + N * d) + 4.0 * N * qkv)),
+        "gemm_o": (nl * 2.0 * N * qd * d, nl * (es * (d * qd + N * qd) + 8.0 * N * d)),
+        "gemm_gate_up_swiglu": (nl * 2.0 * N * d * 2 * ffn,
+                                nl * es * (2.0 * ffn * d + N * d + N * ffn)),
+        "gemm_down": (nl * 2.0 * N * ffn * d, nl * (es * (d * ffn + N * ffn) + 8.0 * N * d)),
+        "attention": (nl * 4.0 * qk * hq * dh, nl * es * (2.0 * N * qd + 2.0 * keys * hkv * dh)),
         "lm_head": (2.0 * m_rows * d * V, es * (V * d + m_rows * d)),
     }
-    return w
 
 
-def step_work(shape, n_rows, seq_len, m_rows):
-    """Whole-step algorithmic FLOPs and bytes (weights read once, KV read and
-    written once, logits never stored)."""
+def step_work(shape, rows, m_rows):
+    """Whole-step algorithmic FLOPs and bytes: weights read once, every key and
+    value read once and every recomputed row's written once, logits never stored."""
     d, dh, hq, hkv, ffn, V, nl = (shape.d_model, shape.head_dim, shape.n_q_heads,
                                   shape.n_kv_heads, shape.d_ffn, shape.vocab, shape.n_layers)
     es = 2 if shape.dtype == "bf16" else 4
     p_lay = d * (hq + 2 * hkv) * dh + hq * dh * d + 3 * d * ffn
-    F = 2.0 * n_rows * nl * p_lay + 4.0 * nl * hq * dh * n_rows * seq_len + 2.0 * m_rows * d * V
+    N = sum(n for n, _ in rows)
+    F = 2.0 * N * nl * p_lay + 4.0 * nl * hq * dh * sum(n * L for n, L in rows) \
+        + 2.0 * m_rows * d * V
     kv_row = 2 * nl * hkv * dh * es
-    B = es * (nl * p_lay + V * d) + kv_row * (seq_len + n_rows)
+    B = es * (nl * p_lay + V * d) + kv_row * (sum(L for _, L in rows) + N)
     return F, B
 
 
-def cpu_baseline(cfg, tensors, prompt, G, inv_tau, n_sample_layers):
-    """Time the oracle (fp64 NumPy) on a bounded sample of one step: the first
-    n_sample_layers layers over all rows plus the LM head and confidence of the
-    block's 32 masked rows; scaled to a whole step (layers x n_layers / n)."""
-    import numpy as np
+def cpu_baseline(cfg, tensors, prompt, G, block, inv_tau, n_sample_layers):
+    """Time the oracle (fp64 NumPy) on a bounded sample of one no-cache step of
+    one request: the first n_sample_layers layers over all rows plus the LM head
+    and confidence of the block's masked rows; scaled to a whole step (layer time
+    x n_layers / n)."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -100,7 +121,7 @@ def cpu_baseline(cfg, tensors, prompt, G, inv_tau, n_sample_layers):
     except Exception:
         threads = None
     f = lambda t: t.float().cpu().numpy()
-    d, dh = cfg.d_model, cfg.head_dim
+    dh = cfg.head_dim
     qd, kd = cfg.n_q_heads * dh, cfg.n_kv_heads * dh
     layers = []
     for l in range(n_sample_layers):
@@ -112,7 +133,7 @@ def cpu_baseline(cfg, tensors, prompt, G, inv_tau, n_sample_layers):
                        "ffn_norm": f(t["ffn_norm"])})
     W = oracle.Weights({"embed": f(tensors["embed"]), "lm_head": f(tensors["lm_head"]),
                         "final_norm": f(tensors["final_norm"])}, layers=layers)
-    req = oracle.Request.new(prompt, G, 32, 0.9, cfg.mask_id)
+    req = oracle.Request.new(prompt, G, block, 0.9, cfg.mask_id)
     L = req.seq_len
     oracle.ensure_cache(cfg, req, n_sample_layers)
     t0 = time.perf_counter()
@@ -134,11 +155,18 @@ def cpu_baseline(cfg, tensors, prompt, G, inv_tau, n_sample_layers):
             "measured_s": t2 - t0}
 
 
+WORKLOADS = {"c2": "C2", "c3-dual": "C3_DUAL", "c3-prefix": "C3_PREFIX", "c4": "C4",
+             "c5": "C5"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--threshold", type=float, default=None,
+                    help="override every request's threshold (the GQA sweep)")
     ap.add_argument("--cpu-layers", type=int, default=4,
                     help="layers of the CPU oracle sample (0 disables the CPU baseline)")
     ap.add_argument("--inv-tau", type=float, default=None,
@@ -155,7 +183,6 @@ def main():
               "copies of this benchmark.", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
     if args.copy_probe:
         n = args.copy_probe << 20
@@ -170,45 +197,78 @@ def main():
     import synth.device as sdev
     from paper_2606_29094_amd import dlm, engine
 
-    w = synth.C2
+    w = getattr(synth, WORKLOADS[args.workload])
     cfg = w.model
     if args.inv_tau is not None:
         inv_tau, tau_src = args.inv_tau, "command line"
     else:
         inv_tau, tau_src = load_inv_tau(cfg.name)
-    dev = torch.device("cuda:0")
     tensors = sdev.model_tensors(cfg)
     shape = engine.ModelShape.of(cfg)
     model = engine.DeviceModel(shape, tensors, inv_tau)
-    prompt, G, thr = synth.request(w, 0)
-    L = len(prompt) + G
-    eng = engine.Engine(model, 1, L, w.cache_mode)
-    req = engine.Request(prompt, G, w.block, thr)
-    eng.admit(req, cfg.mask_id)
 
-    def one_step():
-        nonlocal req
-        if req.done:
-            eng.release(req)
-            req = engine.Request(prompt, G, w.block, thr)
-            eng.admit(req, cfg.mask_id)
-        m = req.masked_in_block
-        n = eng.step([req])[0]
-        return m, n
+    # request stream per slot: the fixed workloads repeat their requests, the
+    # heterogeneous one walks through request ids slot, slot + B, ...
+    B = w.batch
+    hetero = w.prompt_range is not None
+    next_id = [b for b in range(B)]
+
+    def make(slot):
+        rid = next_id[slot]
+        prompt, G, thr = synth.request(w, rid)
+        if hetero:
+            next_id[slot] += B
+        if args.threshold is not None:
+            thr = args.threshold
+        return engine.Request(prompt, G, w.block, thr)
+
+    if hetero:
+        max_len = w.prompt_range[1] + max(w.gen_choices)
+    else:
+        max_len = w.prompt_len + w.gen_len
+    eng = engine.Engine(model, B, max_len, w.cache_mode, max_rows=B * max_len)
+    slots = []
+    for b in range(B):
+        r = make(b)
+        eng.admit(r, cfg.mask_id)
+        slots.append(r)
+
+    stats = {"masked": 0, "unmasked": 0, "F": 0.0, "B": 0.0, "refresh_reqs": 0, "rows": 0,
+             "cls": {}}
+
+    def one_step(account):
+        for b in range(B):
+            if slots[b].done:
+                eng.release(slots[b])
+                slots[b] = make(b)
+                eng.admit(slots[b], cfg.mask_id)
+        rows = step_rows(slots, w.cache_mode)
+        m = sum(r.masked_in_block for r in slots)
+        refresh = sum(1 for r in slots
+                      if w.cache_mode == "none" or r.refreshed_block != r.block_start)
+        counts = eng.step(slots)
+        if account:
+            stats["masked"] += m
+            stats["unmasked"] += sum(counts)
+            stats["refresh_reqs"] += refresh
+            stats["rows"] += sum(n for n, _ in rows)
+            F, Bb = step_work(shape, rows, m)
+            stats["F"] += F
+            stats["B"] += Bb
+            for k, (f, bb) in class_work(shape, rows, m).items():
+                a = stats["cls"].setdefault(k, [0.0, 0.0])
+                a[0] += f
+                a[1] += bb
 
     for _ in range(args.warmup):
-        one_step()
+        one_step(False)
     torch.cuda.synchronize()
     if not args.no_profile:
         dlm.profile_read(model.handle)          # drop anything pending
         dlm.profile_enable(model.handle, True)
-    masked_rows = 0
-    unmasked = 0
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        m, n = one_step()
-        masked_rows += m
-        unmasked += n
+        one_step(True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     prof = {}
@@ -216,64 +276,75 @@ def main():
         dlm.profile_enable(model.handle, False)
         prof = dlm.profile_read(model.handle)
     elapsed = t1 - t0
-    ms_per_step = 1e3 * elapsed / args.steps
+    t_step = elapsed / args.steps
+    peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_F32_TFLOPS
+    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
 
-    # roofline of the dominant kernel (largest total event time)
-    m_avg = masked_rows / args.steps
-    work = kernel_work(shape, L, L, m_avg)
     kernels = {}
     for name, (calls, tot) in prof.items():
-        avg_ms = tot / max(calls, 1)
-        entry = {"calls": calls, "avg_us": 1e3 * avg_ms, "share": tot / (1e3 * elapsed)}
-        if name in work:
-            F, B = work[name]
-            entry["tflops"] = F / (avg_ms * 1e-3) / 1e12
-            entry["gbs"] = B / (avg_ms * 1e-3) / 1e9
+        entry = {"calls": calls, "avg_us": 1e3 * tot / max(calls, 1),
+                 "share": tot / (1e3 * elapsed)}
+        if name in stats["cls"]:
+            F, Bb = stats["cls"][name]
+            entry["tflops"] = F / (tot * 1e-3) / 1e12
+            entry["gbs"] = Bb / (tot * 1e-3) / 1e9
         kernels[name] = entry
     roof = None
-    if prof:
-        dom = max((k for k in prof if k in work), key=lambda k: prof[k][1])
-        F, B = work[dom]
-        avg_s = prof[dom][1] / prof[dom][0] * 1e-3
-        peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_F32_TFLOPS
-        traffic, traffic_src = measured_traffic(dom)
-        ai = F / B
-        if ai >= peak * 1e12 / (PEAK_HBM_GBS * 1e9):
-            achieved = F / avg_s / 1e12
+    timed = [k for k in prof if k in stats["cls"]]
+    if timed:
+        dom = max(timed, key=lambda k: prof[k][1])
+        calls, tot = prof[dom]
+        F, Bb = stats["cls"][dom]
+        F1, B1 = F / calls, Bb / calls                 # per launch
+        avg_s = tot / calls * 1e-3
+        traffic, traffic_src = measured_traffic(dom) if args.workload == "c2" else (None, None)
+        if F1 / B1 >= ridge:
+            achieved = F1 / avg_s / 1e12
             roof = {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": peak,
                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": traffic,
-                    "traffic_source": traffic_src, "algorithmic_bytes": B,
-                    "flop_per_launch": F, "avg_launch_us": avg_s * 1e6}
+                    "traffic_source": traffic_src, "algorithmic_bytes": B1,
+                    "flop_per_launch": F1, "avg_launch_us": avg_s * 1e6}
         else:
-            achieved = B / avg_s / 1e9
+            achieved = B1 / avg_s / 1e9
             roof = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
-                    "traffic_source": traffic_src, "bytes_per_launch": B,
+                    "traffic_source": traffic_src, "bytes_per_launch": B1,
                     "avg_launch_us": avg_s * 1e6}
-    Fs, Bs = step_work(shape, L, L, m_avg)
-    t_step = elapsed / args.steps
+    Fs, Bs = stats["F"] / args.steps, stats["B"] / args.steps
     step_roof = {"tflops": Fs / t_step / 1e12, "gbs": Bs / t_step / 1e9,
-                 "frac_mfma": Fs / t_step / (PEAK_BF16_TFLOPS * 1e12),
+                 "frac_mfma": Fs / t_step / (peak * 1e12),
                  "frac_hbm": Bs / t_step / (PEAK_HBM_GBS * 1e9),
+                 "bound": "mfma" if Fs / Bs >= ridge else "hbm",
                  "flop_per_step": Fs, "bytes_per_step": Bs}
 
     cpu = None
     if args.cpu_layers > 0:
-        cpu = cpu_baseline(cfg, tensors, prompt, G, inv_tau, args.cpu_layers)
+        prompt, G, _ = synth.request(w, 0)
+        cpu = cpu_baseline(cfg, tensors, prompt, G, w.block, inv_tau, args.cpu_layers)
+        if B > 1 or w.cache_mode != "none":
+            cpu["sample"] += ("; one request's no-cache step (the timed GPU steps batch "
+                              f"{B} requests, cache mode {w.cache_mode})")
 
     out = {
         "metric": "denoise steps/s + unmasked tokens/s per MI355X; % MFMA / HBM roofline",
         "value": args.steps / elapsed,
         "unit": "steps/s",
-        "unmasked_tokens_per_s": unmasked / elapsed,
+        "unmasked_tokens_per_s": stats["unmasked"] / elapsed,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": w.name, "batch": w.batch, "prompt_len": w.prompt_len,
-                   "gen_len": w.gen_len, "block": w.block, "cache": w.cache_mode,
-                   "threshold": w.threshold, "inv_tau": inv_tau, "inv_tau_source": tau_src,
-                   "weights": "synthetic N(0,0.02) seed 0", "recomputed_rows": L,
-                   "avg_masked_rows": m_avg},
+        "ms_per_step": 1e3 * t_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if shape.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B,
+                   "prompt_len": w.prompt_len or list(w.prompt_range),
+                   "gen_len": w.gen_len or list(w.gen_choices),
+                   "block": w.block, "cache": w.cache_mode,
+                   "threshold": args.threshold if args.threshold is not None else
+                   (list(w.threshold_choices) if hetero else w.threshold),
+                   "inv_tau": inv_tau, "inv_tau_source": tau_src,
+                   "weights": "synthetic N(0,0.02) seed 0",
+                   "avg_recomputed_rows": stats["rows"] / args.steps,
+                   "avg_masked_rows": stats["masked"] / args.steps,
+                   "avg_refresh_requests": stats["refresh_reqs"] / args.steps},
         "roofline": roof,
         "step_roofline": step_roof,
         "kernels": kernels,
