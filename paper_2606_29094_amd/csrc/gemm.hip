@@ -42,6 +42,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  if (epi.skip_tile(m0)) return;   // uniform over the block
   const int kbeg = blockIdx.z * k_per_split;
   const int kend = min(K, kbeg + k_per_split);
   const int nkt = kend > kbeg ? ceil_div(kend - kbeg, BK) : 0;
@@ -258,9 +259,10 @@ int lm_head_tiles(const GemmPlan& p, int V) {
 
 template <typename T>
 hipError_t gemm_lm_head(const GemmPlan& p, const T* U, int ldu, const T* W, int M, int V, int K,
-                        float inv_tau, float* pm, float* ps, int* pi, int ld, hipStream_t st) {
+                        float inv_tau, float* pm, float* ps, int* pi, int ld,
+                        const int* m_count, hipStream_t st) {
   if (p.splits != 1) return hipErrorInvalidValue;
-  EpiLMHead e{pm, ps, pi, M, V, inv_tau, ld};
+  EpiLMHead e{pm, ps, pi, M, V, inv_tau, ld, m_count};
   return launch<T>(p, U, ldu, W, K, M, V, K, e, st);
 }
 
@@ -274,7 +276,7 @@ hipError_t gemm_lm_head(const GemmPlan& p, const T* U, int ldu, const T* W, int 
   template hipError_t gemm_swiglu<T>(const GemmPlan&, const T*, int, const T*, int, int, int,    \
                                      int, T*, int, hipStream_t);                                \
   template hipError_t gemm_lm_head<T>(const GemmPlan&, const T*, int, const T*, int, int, int,   \
-                                      float, float*, float*, int*, int, hipStream_t);
+                                      float, float*, float*, int*, int, const int*, hipStream_t);
 INST(bf16)
 INST(float)
 

@@ -34,6 +34,7 @@ constexpr int kLdsRow = kRowBytes + 16; // padded LDS row stride
 struct EpiStore {
   float* C; int ldc; long split_stride; int M, N;
   __device__ int b_row(int n) const { return n; }
+  __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int) const {
@@ -56,6 +57,7 @@ struct EpiStore {
 struct EpiScaledStore {
   float* C; int ldc; int M, N; float scale;
   __device__ int b_row(int n) const { return n; }
+  __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int) const {
@@ -77,6 +79,7 @@ struct EpiScaledStore {
 struct EpiAdd {
   float* C; int ldc; int M, N;
   __device__ int b_row(int n) const { return n; }
+  __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int) const {
@@ -105,6 +108,7 @@ struct EpiSwiGLU {
     int f = (n >> 5) * 16 + (n & 15);
     return ((n >> 4) & 1) ? F + f : f;
   }
+  __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int) const {
@@ -141,10 +145,14 @@ __device__ __forceinline__ RowStat combine(RowStat a, RowStat b) {
 }
 
 // Fused LM head: per row and vocab tile, (max, sum exp(z - max), lowest argmax)
-// of z = acc * inv_tau; written to part_[m|s|i][tile][row].
+// of z = acc * inv_tau; written to part_[m|s|i][tile][row]. When m_count is
+// given (the device-side number of rows that need a prediction, packed first),
+// row tiles at or beyond it are skipped.
 struct EpiLMHead {
   float* pm; float* ps; int* pi; int M; int V; float inv_tau; int ld;  // ld = rows stride
+  const int* m_count;
   __device__ int b_row(int n) const { return n; }
+  __device__ bool skip_tile(int m0) const { return m_count && m0 >= *m_count; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int wave_n,
                              char* smem, int waves_n, int bm) const {

@@ -47,6 +47,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  if (epi.skip_tile(m0)) return;   // uniform over the block
   const int kbeg = blockIdx.z * k_per_split;
   const int kend = min(K, kbeg + k_per_split);
   const int nkt = kend > kbeg ? (kend - kbeg) / BK : 0;

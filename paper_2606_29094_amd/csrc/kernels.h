@@ -64,7 +64,8 @@ hipError_t gemm_swiglu(const GemmPlan& p, const T* A, int lda, const T* W, int l
 int lm_head_tiles(const GemmPlan& p, int V);
 template <typename T>
 hipError_t gemm_lm_head(const GemmPlan& p, const T* U, int ldu, const T* W, int M, int V, int K,
-                        float inv_tau, float* pm, float* ps, int* pi, int ld, hipStream_t st);
+                        float inv_tau, float* pm, float* ps, int* pi, int ld,
+                        const int* m_count, hipStream_t st);
 
 // ---- per-row kernels (rowwise.hip) ----
 template <typename T>

@@ -369,7 +369,7 @@ dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPl
   float* conf = reinterpret_cast<float*>(ws + L.conf);
   int* tok = reinterpret_cast<int*>(ws + L.tok);
   LAUNCH(m, st, "lm_head", gemm_lm_head<T>(L.g_lm, u, d, reinterpret_cast<const T*>(m->lm_head), m_max, cf.vocab, d,
-                           cf.inv_tau, pm, ps, pi, L.m_max, st));
+                           cf.inv_tau, pm, ps, pi, L.m_max, lm_count, st));
   LAUNCH(m, st, "lm_combine", lm_combine(pm, ps, pi, L.tiles, L.m_max, lm_count, m_max, conf, tok, st));
   LAUNCH(m, st, "unmask", unmask_select(p, conf, tok, req_off, b->tokens, b->mask, out->n_unmasked, out->pos,
                          out->tok, out->conf, out->block_conf, out->block_tok, st));
@@ -622,11 +622,11 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
   if (cf.dtype == DLM_BF16) {
     HIPCHECK(gemm_lm_head<bf16>(gp, reinterpret_cast<const bf16*>(u_rows), cf.d_model,
                                 reinterpret_cast<const bf16*>(m->lm_head), m_rows, cf.vocab,
-                                cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, st));
+                                cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, cnt, st));
   } else {
     HIPCHECK(gemm_lm_head<float>(gp, reinterpret_cast<const float*>(u_rows), cf.d_model,
                                  reinterpret_cast<const float*>(m->lm_head), m_rows, cf.vocab,
-                                 cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, st));
+                                 cf.d_model, cf.inv_tau, pm, ps, pi, m_rows, cnt, st));
   }
   HIPCHECK(lm_combine(pm, ps, pi, tiles, m_rows, cnt, m_rows, conf, tok, st));
   return DLM_OK;
