@@ -83,8 +83,6 @@ template <typename T>
 hipError_t qkv_rope_scatter(const StepPlan& p, const float* qkv, int splits, long split_stride,
                             const float2* cs, int hq, int hkv, int dh, T* q_out,
                             T* kcache, T* vcache, int s_max, hipStream_t st);
-hipError_t add_partials(const float* part, int splits, long split_stride, int n, int d, float* h,
-                        hipStream_t st);
 hipError_t lm_select_rows(const StepPlan& p, const uint8_t* mask, int all_rows, int* lm_rows,
                           int* lm_count, int* req_lm_off, int* req_lm_cnt, hipStream_t st);
 template <typename T>

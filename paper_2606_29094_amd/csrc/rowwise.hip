@@ -238,33 +238,6 @@ hipError_t qkv_rope_scatter(const StepPlan& p, const float* qkv, int splits, lon
   return hipGetLastError();
 }
 
-// ------------------------------------------------------ split-K reduction --
-// h[n][j] += sum_s part[s][n][j], slices summed in order s = 0, 1, ...
-__global__ void add_partials_kernel(const float* __restrict__ part, int splits, long stride,
-                                    long total4, float* __restrict__ h) {
-  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < total4;
-       i += (long)gridDim.x * blockDim.x) {
-    float4 acc = reinterpret_cast<const float4*>(part)[i];
-    for (int s = 1; s < splits; ++s) {
-      float4 v = reinterpret_cast<const float4*>(part + s * stride)[i];
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-    }
-    float4 o = reinterpret_cast<float4*>(h)[i];
-    o.x += acc.x; o.y += acc.y; o.z += acc.z; o.w += acc.w;
-    reinterpret_cast<float4*>(h)[i] = o;
-  }
-}
-
-hipError_t add_partials(const float* part, int splits, long split_stride, int n, int d, float* h,
-                        hipStream_t st) {
-  long total4 = (long)n * d / 4;
-  if (total4 == 0) return hipSuccess;
-  int blocks = (int)std::min<long>((total4 + 255) / 256, 4096);
-  hipLaunchKernelGGL(add_partials_kernel, dim3(blocks), dim3(256), 0, st, part, splits,
-                     split_stride, total4, h);
-  return hipGetLastError();
-}
-
 // ----------------------------------------------------- LM row selection --
 // Rows that get a prediction: the masked positions of each active block
 // (all block positions when all_rows != 0), in request order, ascending
