@@ -188,16 +188,17 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
                                size_t ws_bytes, void* stream);
 
 /* Kernel timing. While enabled, every kernel the library enqueues for this
- * model is bracketed by a pair of HIP events on the launch stream.
- * dlm_profile_read waits for those events, adds their elapsed times per kernel
- * class into out[0 .. *n_out) (at most cap entries, in first-seen order) and
- * clears them. Timing adds two event records per kernel launch. */
+ * model (or, when only_class is not NULL, every kernel of that class) is
+ * bracketed by a pair of HIP events on the launch stream. dlm_profile_read
+ * waits for those events, adds their elapsed times per kernel class into
+ * out[0 .. *n_out) (at most cap entries, in first-seen order) and clears them.
+ * Each timed launch costs two event records on the host. */
 typedef struct dlm_profile_entry {
   char name[32];          /* kernel class, e.g. "gemm_gate_up_swiglu"                  */
   int32_t calls;          /* launches timed                                             */
   double total_ms;        /* sum of their event-to-event times                          */
 } dlm_profile_entry;
-dlm_status dlm_profile_enable(dlm_model* m, int32_t on);
+dlm_status dlm_profile_enable(dlm_model* m, int32_t on, const char* only_class);
 dlm_status dlm_profile_read(dlm_model* m, dlm_profile_entry* out, int32_t cap, int32_t* n_out);
 
 /* Message for the last non-OK status on this thread ("" if none). */

@@ -47,13 +47,14 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
   do {                                                                            \
     Profiler& pf_ = (model)->prof;                                                \
     hipEvent_t a_ = nullptr, b_ = nullptr;                                        \
-    if (pf_.on) {                                                                 \
+    const bool t_ = pf_.wants(name);                                              \
+    if (t_) {                                                                     \
       a_ = pf_.take();                                                            \
       b_ = pf_.take();                                                            \
       if (a_) (void)hipEventRecord(a_, stream);                                   \
     }                                                                             \
     HIPCHECK(expr);                                                               \
-    if (pf_.on && a_ && b_) {                                                     \
+    if (t_ && a_ && b_) {                                                         \
       (void)hipEventRecord(b_, stream);                                           \
       pf_.pending.push_back({pf_.kind_of(name), a_, b_});                         \
     }                                                                             \
@@ -62,6 +63,8 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Per-kernel-class event timing (dlm_profile_*).
 struct Profiler {
   bool on = false;
+  std::string only;        // empty: every class
+  bool wants(const char* n) const { return on && (only.empty() || only == n); }
   struct Rec { int kind; hipEvent_t a, b; };
   std::vector<Rec> pending;
   std::vector<hipEvent_t> pool;
@@ -445,10 +448,11 @@ dlm_status dlm_load_weights(const dlm_config* cfg, const dlm_weights* w, dlm_mod
 
 void dlm_model_destroy(dlm_model* m) { delete m; }
 
-dlm_status dlm_profile_enable(dlm_model* m, int32_t on) {
+dlm_status dlm_profile_enable(dlm_model* m, int32_t on, const char* only_class) {
   g_err.clear();
   if (!m) return fail(DLM_EINVAL, "model is NULL");
   m->prof.on = on != 0;
+  m->prof.only = only_class ? only_class : "";
   return DLM_OK;
 }
 

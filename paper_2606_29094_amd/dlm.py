@@ -98,7 +98,7 @@ def lib():
                                        c_void_p, c_size_t, c_void_p]
         L.dlm_head_confidence.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p]
-        L.dlm_profile_enable.argtypes = [c_void_p, c_int32]
+        L.dlm_profile_enable.argtypes = [c_void_p, c_int32, ctypes.c_char_p]
         L.dlm_profile_read.argtypes = [c_void_p, POINTER(DlmProfileEntry), c_int32,
                                        POINTER(c_int32)]
         L.dlm_last_error.argtypes = []
@@ -206,8 +206,9 @@ def head_confidence(model, u_rows, m_rows: int, conf, tok, workspace, stream=Non
                                     _stream(stream)))
 
 
-def profile_enable(model, on: bool):
-    check(lib().dlm_profile_enable(model, 1 if on else 0))
+def profile_enable(model, on: bool, only_class: str | None = None):
+    check(lib().dlm_profile_enable(model, 1 if on else 0,
+                                   None if only_class is None else only_class.encode()))
 
 
 def profile_read(model, cap: int = 64) -> dict:
