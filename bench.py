@@ -174,6 +174,9 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 10 device-to-device copies of MIB MiB (calibrates the "
                          "HBM byte counters) and exit")
+    ap.add_argument("--profile-steps", type=int, default=10,
+                    help="untimed steps after the warm-up with every kernel class timed "
+                         "(per-class breakdown, choice of the dominant kernel)")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-kernel event records")
     args = ap.parse_args()
@@ -260,17 +263,20 @@ def main():
                 a[0] += f
                 a[1] += bb
 
-    # warm-up: every kernel class timed (untimed steps) to find the dominant
-    # class and give the per-class breakdown; the timed steps then bracket only
-    # the dominant class with events, so the timing does not slow the host side
-    warm_prof = {}
-    if not args.no_profile:
-        dlm.profile_enable(model.handle, True)
+    # warm-up (untimed), then untimed profile steps with every kernel class
+    # bracketed by events (the per-class breakdown of the steady state and the
+    # dominant class); the timed steps then bracket only the dominant class, so
+    # the events do not slow the host side of the timed steps
     for _ in range(args.warmup):
         one_step(False)
     torch.cuda.synchronize()
+    warm_prof = {}
     dom = None
     if not args.no_profile:
+        dlm.profile_enable(model.handle, True)
+        for _ in range(args.profile_steps):
+            one_step(False)
+        torch.cuda.synchronize()
         dlm.profile_enable(model.handle, False)
         warm_prof = dlm.profile_read(model.handle)
         timed_cls = [k for k in warm_prof if k in ("gemm_qkv", "gemm_o", "gemm_gate_up_swiglu",
@@ -292,7 +298,7 @@ def main():
     peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_F32_TFLOPS
     ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
 
-    # per-class breakdown from the warm-up steps (all classes timed there)
+    # per-class breakdown from the profile steps (all classes timed there)
     kernels = {}
     warm_total = sum(t for _, t in warm_prof.values()) or 1.0
     for name, (calls, tot) in warm_prof.items():
@@ -338,6 +344,7 @@ def main():
         "unit": "steps/s",
         "unmasked_tokens_per_s": stats["unmasked"] / elapsed,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "profile_steps": 0 if args.no_profile else args.profile_steps,
         "ms_per_step": 1e3 * t_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16" if shape.dtype == "bf16" else "f32",
         "data": "synthetic",
@@ -354,7 +361,7 @@ def main():
                    "avg_refresh_requests": stats["refresh_reqs"] / args.steps},
         "roofline": roof,
         "step_roofline": step_roof,
-        "kernels_warmup": kernels,
+        "kernels_profiled": kernels,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -2,9 +2,10 @@
 // cached key/value position of their request's slot: O = softmax(Q K^T /
 // sqrt(dh)) V per query head; query head h reads key/value head h / (Hq/Hkv).
 //
-// bf16 path (matrix cores): one block = 64 query rows of one request x one
-// query head, 4 waves of 16 rows. Key tiles of 64 positions are staged in LDS
-// (keys row-major, values transposed, which is how the cache stores them).
+// bf16 path (matrix cores): one block = 32 or 64 query rows of one request x
+// one query head; waves split the rows in groups of 16 and the keys in two
+// groups (see attn_bf16_kernel). Key tiles are staged in LDS (keys row-major,
+// values transposed, which is how the cache stores them).
 // Each wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (keys as the A
 // operand, its 16 query rows as B, held in registers), so that every lane
 // ends up owning one query and 16 keys: the online softmax needs only two
@@ -19,38 +20,66 @@
 #include "common.h"
 #include "kernels.h"
 
+#ifndef ATTN_PLO
+#define ATTN_PLO 1
+#endif
+
 namespace dlm {
 
 constexpr int kKeyTile = 64;
+constexpr bool kPLo = ATTN_PLO;
 
-template <int DH>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* __restrict__ q,
-                                                        const bf16* __restrict__ kc,
-                                                        const bf16* __restrict__ vc, int s_max,
-                                                        int hq, int hkv, bf16* __restrict__ out,
-                                                        float scale_log2) {
-  constexpr int KS = DH + 8;            // K tile row stride (elements)
-  constexpr int VS = kKeyTile + 8;      // V^T tile row stride (elements)
-  constexpr int NDB = DH / 16;          // output dh blocks
-  constexpr int NKS = DH / 32;          // k steps of S
-  __shared__ __attribute__((aligned(16))) bf16 ks[kKeyTile * KS];
+// Wave layout: QG query groups of 16 rows x KG key groups. A block stages
+// key tiles of 64 * KG positions; key group kg works on keys [64 kg, 64 kg +
+// 64) of each tile. Each wave keeps its own online-softmax state; the key
+// groups are merged in LDS at the end (rescaling by the group maxima), so the
+// result is the same softmax over all keys.
+//
+// Softmax bookkeeping per query: m is a reference maximum of the raw scores,
+// l and O^T are kept relative to 2^((s - m) c) with c = log2(e) / sqrt(dh).
+// m is only moved (and l, O^T rescaled) when a tile's maximum exceeds it by
+// more than 8 / c, so the weights stay below 2^8 and most tiles skip the
+// rescale; the normalised result is the same.
+// PLO: P is fed to the PV product as two bf16 terms (P = P_hi + P_lo, about
+// 16 significant bits, two MFMAs per block) instead of one.
+template <int DH, int QG, int KG, bool PLO>
+__global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, const bf16* __restrict__ q,
+                                                               const bf16* __restrict__ kc,
+                                                               const bf16* __restrict__ vc,
+                                                               int s_max, int hq, int hkv,
+                                                               bf16* __restrict__ out,
+                                                               float scale_log2) {
+  constexpr int NT = QG * KG * 64;
+  constexpr int QT = 16 * QG;             // query rows per block
+  constexpr int SK = 64 * KG;             // keys per staged tile
+  constexpr int KS = DH + 8;              // K tile row stride (elements)
+  constexpr int VS = SK + 8;              // V^T tile row stride (elements)
+  constexpr int NDB = DH / 16;            // output dh blocks
+  constexpr int NKS = DH / 32;            // k steps of S
+  __shared__ __attribute__((aligned(16))) bf16 ks[SK * KS];
   __shared__ __attribute__((aligned(16))) bf16 vs[DH * VS];
 
-  // head-major grid: consecutive blocks (which the dispatcher spreads over the
-  // XCDs round-robin) are different heads, so the query tiles of one head
-  // (same K/V) land on the same XCD and share its L2
+  // head-major grid: consecutive blocks (spread over the XCDs round-robin) are
+  // different heads, so the query tiles of one head share one XCD's L2
   const int h = blockIdx.x, tile = blockIdx.y;
-  const int r = plan_req_of_tile(p, tile);
+  // request of this tile: tiles of QT rows are numbered request by request
+  int r = 0, t0 = 0;
+  for (; r + 1 < p.n_req; ++r) {
+    const int nt = (p.r[r].nrows + QT - 1) / QT;
+    if (tile < t0 + nt) break;
+    t0 += nt;
+  }
   const ReqPlan& rq = p.r[r];
-  const int lrow0 = (tile - rq.tile0) * kQTile;
-  const int nvalid = min(kQTile, rq.nrows - lrow0);
+  const int lrow0 = (tile - t0) * QT;
+  const int nvalid = min(QT, rq.nrows - lrow0);
   const int L = rq.seq_len;
   const int kvh = h / (hq / hkv);
   const bf16* kb = kc + ((long)(rq.slot * hkv + kvh) * s_max) * DH;
   const bf16* vb = vc + ((long)(rq.slot * hkv + kvh) * DH) * s_max;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int qr = wave * 16 + (lane & 15);          // query row of this lane in the tile
+  const int qg = wave % QG, kg = wave / QG;
+  const int qr = qg * 16 + (lane & 15);           // query row of this lane in the tile
   const bool q_ok = qr < nvalid;
   const long qrow = rq.row0 + lrow0 + qr;
   const int g = lane >> 4;
@@ -68,104 +97,129 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* 
   f32x4 o[NDB];
 #pragma unroll
   for (int i = 0; i < NDB; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_ref = -INFINITY, l_run = 0.f;
 
   // K/V^T tiles go through registers: the next tile's global loads are issued
   // before the current tile's MFMAs and written to LDS after them.
-  constexpr int KCH = kKeyTile * (DH / 8) / 256;   // 16-byte K chunks per thread
-  constexpr int VCH = DH * (kKeyTile / 8) / 256;   // 16-byte V^T chunks per thread
+  constexpr int KCH = SK * (DH / 8) / NT;   // 16-byte K chunks per thread
+  constexpr int VCH = DH * (SK / 8) / NT;   // 16-byte V^T chunks per thread
+  static_assert(KCH * NT == SK * (DH / 8) && VCH * NT == DH * (SK / 8), "tile split");
   u32x4 kreg[KCH], vreg[VCH];
   auto load_tile = [&](int key0) {
+    if (key0 + SK <= L) {                       // whole tile inside the sequence
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + i * 256;
-      const int kk = c / (DH / 8), cc = c % (DH / 8);
-      kreg[i] = key0 + kk < L
-                    ? *reinterpret_cast<const u32x4*>(kb + (long)(key0 + kk) * DH + cc * 8)
-                    : u32x4{0u, 0u, 0u, 0u};
-    }
+      for (int i = 0; i < KCH; ++i) {
+        const int c = tid + i * NT;
+        kreg[i] = *reinterpret_cast<const u32x4*>(kb + (long)(key0 + c / (DH / 8)) * DH +
+                                                  (c % (DH / 8)) * 8);
+      }
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = tid + i * 256;
-      const int d = c / (kKeyTile / 8), cc = c % (kKeyTile / 8);
-      const int kk0 = key0 + cc * 8;
-      const bf16* src = vb + (long)d * s_max + kk0;
-      if (kk0 + 8 <= L) {
-        vreg[i] = *reinterpret_cast<const u32x4*>(src);
-      } else {
-        bf16 tmp[8];
+      for (int i = 0; i < VCH; ++i) {
+        const int c = tid + i * NT;
+        vreg[i] = *reinterpret_cast<const u32x4*>(vb + (long)(c / (SK / 8)) * s_max + key0 +
+                                                  (c % (SK / 8)) * 8);
+      }
+    } else {
+      // last tile: keys >= L read as zero. A V^T chunk starting below L lies
+      // inside the slot (L <= s_max, both chunk start and s_max multiples of
+      // 8); its values at keys >= L are cleared.
 #pragma unroll
-        for (int e = 0; e < 8; ++e) tmp[e] = (kk0 + e < L) ? src[e] : (bf16)0.0f;
-        vreg[i] = *reinterpret_cast<const u32x4*>(tmp);
+      for (int i = 0; i < KCH; ++i) {
+        const int c = tid + i * NT;
+        const int kk = key0 + c / (DH / 8);
+        kreg[i] = kk < L ? *reinterpret_cast<const u32x4*>(kb + (long)kk * DH + (c % (DH / 8)) * 8)
+                         : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int i = 0; i < VCH; ++i) {
+        const int c = tid + i * NT;
+        const int kk0 = key0 + (c % (SK / 8)) * 8;
+        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+        if (kk0 < L) {
+          v = *reinterpret_cast<const u32x4*>(vb + (long)(c / (SK / 8)) * s_max + kk0);
+          const int n = L - kk0;                // valid keys in this chunk (> 0)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t keep = (2 * w < n ? 0x0000ffffu : 0u) | (2 * w + 1 < n ? 0xffff0000u : 0u);
+            v[w] &= keep;
+          }
+        }
+        vreg[i] = v;
       }
     }
   };
   auto store_tile = [&]() {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
-      const int c = tid + i * 256;
+      const int c = tid + i * NT;
       *reinterpret_cast<u32x4*>(ks + (c / (DH / 8)) * KS + (c % (DH / 8)) * 8) = kreg[i];
     }
 #pragma unroll
     for (int i = 0; i < VCH; ++i) {
-      const int c = tid + i * 256;
-      *reinterpret_cast<u32x4*>(vs + (c / (kKeyTile / 8)) * VS + (c % (kKeyTile / 8)) * 8) = vreg[i];
+      const int c = tid + i * NT;
+      *reinterpret_cast<u32x4*>(vs + (c / (SK / 8)) * VS + (c % (SK / 8)) * 8) = vreg[i];
     }
   };
 
-  const int ntiles = ceil_div(L, kKeyTile);
+  const int ntiles = ceil_div(L, SK);
   load_tile(0);
   store_tile();
   __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
-    const int key0 = t * kKeyTile;
-    if (t + 1 < ntiles) load_tile(key0 + kKeyTile);
+    const int key0 = t * SK + kg * 64;          // this wave's 64 keys
+    if (t + 1 < ntiles) load_tile((t + 1) * SK);
+    const bf16* ksg = ks + kg * 64 * KS;
 
-    // S^T blocks: sblk[kb][i] = score(key = 16*kb + 4*g + i, query = lane&15)
+    // S^T blocks: sblk[kb][i] = raw score(key = key0 + 16*kb + 4*g + i, query = lane&15)
     f32x4 sblk[4];
 #pragma unroll
     for (int kbk = 0; kbk < 4; ++kbk) {
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(ks + (kbk * 16 + (lane & 15)) * KS + s * 32 + g * 8);
+        const u32x4 a = *reinterpret_cast<const u32x4*>(ksg + (kbk * 16 + (lane & 15)) * KS + s * 32 + g * 8);
         acc = mfma16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, qf[s]), acc);
       }
       sblk[kbk] = acc;
     }
-    // scale (log2 domain) and mask keys beyond L
+    if (t == ntiles - 1) {                      // keys beyond L only in the last tile
+#pragma unroll
+      for (int kbk = 0; kbk < 4; ++kbk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (key0 + kbk * 16 + 4 * g + i >= L) sblk[kbk][i] = -INFINITY;
+    }
     float mt = -INFINITY;
 #pragma unroll
     for (int kbk = 0; kbk < 4; ++kbk)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = key0 + kbk * 16 + 4 * g + i;
-        float v = key < L ? sblk[kbk][i] * scale_log2 : -INFINITY;
-        sblk[kbk][i] = v;
-        mt = fmaxf(mt, v);
-      }
+      for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sblk[kbk][i]);
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = exp2f(m_run - m_new);     // m_run = -inf on the first tile -> 0
+    // move the reference maximum only on a large increase (false while both
+    // are -inf: a key group that has seen no key below L yet)
+    const bool grow = (mt - m_ref) * scale_log2 > 8.0f;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float alpha = grow ? __builtin_amdgcn_exp2f((m_ref - mt) * scale_log2) : 1.0f;
+      if (grow) m_ref = mt;
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < NDB; ++i) o[i] *= alpha;
+    }
+    const float nm = m_ref == -INFINITY ? 0.0f : -m_ref * scale_log2;
     float lsum = 0.f;
 #pragma unroll
     for (int kbk = 0; kbk < 4; ++kbk)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float e = exp2f(sblk[kbk][i] - m_new);
+        const float e = __builtin_amdgcn_exp2f(fmaf(sblk[kbk][i], scale_log2, nm));
         sblk[kbk][i] = e;
         lsum += e;
       }
-    l_run = l_run * alpha + lsum;
-    m_run = m_new;
-#pragma unroll
-    for (int i = 0; i < NDB; ++i) o[i] *= alpha;
+    l_run += lsum;
 
     // O^T += V^T P^T over two 32-key steps; B operand slot 8g+e <-> key
     // 32*j + (e < 4 ? 4g + e : 16 + 4g + e - 4)
-    // P = P_hi + P_lo with both terms bf16: the product with the bf16 values
-    // keeps about 16 bits of P instead of 8 (two MFMAs per block).
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       bf16x8 ph, pl;
@@ -173,16 +227,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* 
       for (int e = 0; e < 8; ++e) {
         const float pv = e < 4 ? sblk[2 * j][e] : sblk[2 * j + 1][e - 4];
         ph[e] = (bf16)pv;
-        pl[e] = (bf16)(pv - (float)ph[e]);
+        if constexpr (PLO) pl[e] = (bf16)(pv - (float)ph[e]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const bf16* vrow = vs + (db * 16 + (lane & 15)) * VS + 32 * j + 4 * g;
+        const bf16* vrow = vs + (db * 16 + (lane & 15)) * VS + kg * 64 + 32 * j + 4 * g;
         const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
         const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
         const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
         o[db] = mfma16_bf16(a, ph, o[db]);
-        o[db] = mfma16_bf16(a, pl, o[db]);
+        if constexpr (PLO) o[db] = mfma16_bf16(a, pl, o[db]);
       }
     }
     if (t + 1 < ntiles) {
@@ -191,6 +245,45 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepPlan p, const bf16* 
       __syncthreads();
     }
   }
+
+  // merge the key groups: groups kg > 0 publish (m, partial l, O^T) in LDS,
+  // group 0 of the same query group rescales and adds them
+  if constexpr (KG > 1) {
+    __syncthreads();                              // K/V tiles no longer needed
+    float* xm = reinterpret_cast<float*>(ks);     // [KG-1][QG][64]
+    float* xl = xm + (KG - 1) * QG * 64;          // [KG-1][QG][64]
+    float* xo = reinterpret_cast<float*>(vs);     // [KG-1][QG][NDB*4][64]
+    static_assert((KG - 1) * QG * 64 * 2 * 4 <= SK * KS * 2, "merge scratch (m, l)");
+    static_assert((KG - 1) * QG * NDB * 4 * 64 * 4 <= DH * VS * 2, "merge scratch (O)");
+    if (kg > 0) {
+      const int slot = (kg - 1) * QG + qg;
+      xm[slot * 64 + lane] = m_ref;
+      xl[slot * 64 + lane] = l_run;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) xo[(slot * NDB * 4 + db * 4 + i) * 64 + lane] = o[db][i];
+    }
+    __syncthreads();
+    if (kg > 0) return;
+#pragma unroll
+    for (int k = 1; k < KG; ++k) {
+      const int slot = (k - 1) * QG + qg;
+      const float m2 = xm[slot * 64 + lane];
+      const float l2 = xl[slot * 64 + lane];
+      const float mm = fmaxf(m_ref, m2);
+      const float a1 = m_ref == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((m_ref - mm) * scale_log2);
+      const float a2 = m2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((m2 - mm) * scale_log2);
+      l_run = l_run * a1 + l2 * a2;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          o[db][i] = o[db][i] * a1 + xo[(slot * NDB * 4 + db * 4 + i) * 64 + lane] * a2;
+      m_ref = mm;
+    }
+  }
+
   // finish: l over the 4 lanes sharing the query, normalise, store
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
@@ -269,21 +362,36 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(StepPlan p, const float* _
   }
 }
 
+template <int DH, int QG, int KG, bool PLO>
+static hipError_t launch_attn(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
+                              int s_max, int hq, int hkv, bf16* out, float scale_log2,
+                              hipStream_t st) {
+  constexpr int QT = 16 * QG;
+  int tiles = 0;
+  for (int r = 0; r < p.n_req; ++r) tiles += (p.r[r].nrows + QT - 1) / QT;
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_bf16_kernel<DH, QG, KG, PLO>), dim3(hq, tiles), dim3(QG * KG * 64), 0, st,
+                     p, q, kc, vc, s_max, hq, hkv, out, scale_log2);
+  return hipGetLastError();
+}
+
+// Query tiles of 32 rows when no request recomputes more than 32 rows (cache
+// steps of blocks <= 32), else 64; two key groups either way.
 template <>
 hipError_t attention<bf16>(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
                            int s_max, int hq, int hkv, int dh, bf16* out, hipStream_t st) {
-  if (p.n_tiles == 0) return hipSuccess;
+  if (p.n_rows == 0) return hipSuccess;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
-  dim3 g(hq, p.n_tiles);
+  int max_rows = 0;
+  for (int r = 0; r < p.n_req; ++r) max_rows = max(max_rows, p.r[r].nrows);
+  const bool small = max_rows <= 32;
   if (dh == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, g, dim3(256), 0, st, p, q, kc, vc, s_max, hq, hkv,
-                       out, scale_log2);
-  else if (dh == 64)
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, g, dim3(256), 0, st, p, q, kc, vc, s_max, hq, hkv,
-                       out, scale_log2);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+    return small ? launch_attn<128, 2, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
+                 : launch_attn<128, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+  if (dh == 64)
+    return small ? launch_attn<64, 2, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
+                 : launch_attn<64, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+  return hipErrorInvalidValue;
 }
 
 template <>
