@@ -159,11 +159,65 @@ WORKLOADS = {"c2": "C2", "c3-dual": "C3_DUAL", "c3-prefix": "C3_PREFIX", "c4": "
              "c5": "C5"}
 
 
+def measure_ceilings(torch, dlm):
+    """Measured chip ceilings: a loop of independent bf16 MFMAs on every CU and
+    a 1 GiB device copy (read + write), best of 3 each, HIP events on the
+    launch stream."""
+    st = torch.cuda.current_stream()
+    out = torch.empty(2048 * 4, dtype=torch.float32, device="cuda:0")
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    best_f, best_c = 0.0, 0.0
+    for _ in range(4):                     # first pass is a warm-up
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record(st)
+        flop = dlm.ceiling_mfma(2048, 512, out.data_ptr(), st.cuda_stream)
+        e1.record(st)
+        dlm.ceiling_copy(src.data_ptr(), dst.data_ptr(), src.numel() * 4, st.cuda_stream)
+        e2.record(st)
+        e2.synchronize()
+        best_f = max(best_f, flop / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+        best_c = max(best_c, 2 * src.numel() * 4 / (e1.elapsed_time(e2) * 1e-3) / 1e9)
+    assert dst[-1].item() == 1.0
+    del src, dst, out
+    torch.cuda.empty_cache()
+    return {"mfma_bf16_tflops": best_f, "copy_gbs": best_c,
+            "method": "2048 blocks x 4 waves x 16384 v_mfma_f32_16x16x32_bf16 (8 independent "
+                      "accumulators per wave); "
+                      "1 GiB device copy, 16-byte lanes (read + write bytes)"}
+
+
+def step_breakdown(per_step):
+    """Per-step-type latency and the distributions of recomputed rows and
+    refreshing requests over the timed steps."""
+    import numpy as np
+    kinds = {}
+    for kind, dt, n, rf in per_step:
+        kinds.setdefault(kind, []).append((dt, n, rf))
+    lat = {}
+    for kind, v in kinds.items():
+        t = np.array([x[0] for x in v]) * 1e3
+        lat[kind] = {"steps": len(v), "mean_ms": float(t.mean()), "median_ms": float(np.median(t)),
+                     "min_ms": float(t.min()), "max_ms": float(t.max()),
+                     "mean_rows": float(np.mean([x[1] for x in v]))}
+    n = np.array([x[2] for x in per_step])
+    rf = np.array([x[3] for x in per_step])
+    q = [0, 25, 50, 75, 100]
+    dist = {"rows_quantiles": {str(k): float(v) for k, v in zip(q, np.percentile(n, q))},
+            "refresh_requests_quantiles": {str(k): float(v) for k, v in
+                                           zip(q, np.percentile(rf, q))},
+            "refresh_requests_hist": {str(int(k)): int(c) for k, c in
+                                      zip(*np.unique(rf, return_counts=True))}}
+    return lat, dist
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=40)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 40; 256 for c4)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default 5; 64 for c4)")
     ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
     ap.add_argument("--threshold", type=float, default=None,
                     help="override every request's threshold (the GQA sweep)")
@@ -179,7 +233,13 @@ def main():
                          "(per-class breakdown, choice of the dominant kernel)")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-kernel event records")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the measured MFMA-loop and copy ceilings")
     args = ap.parse_args()
+    # the heterogeneous stream discards 64 warm-up steps and times 256
+    d_steps, d_warm = (256, 64) if args.workload == "c4" else (40, 5)
+    args.steps = d_steps if args.steps is None else args.steps
+    args.warmup = d_warm if args.warmup is None else args.warmup
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the path is "
               "data-parallel over requests with no exchange, so N GPUs run N independent "
@@ -199,6 +259,8 @@ def main():
     import synth
     import synth.device as sdev
     from paper_2606_29094_amd import dlm, engine
+
+    ceilings = None if args.no_ceilings else measure_ceilings(torch, dlm)
 
     w = getattr(synth, WORKLOADS[args.workload])
     cfg = w.model
@@ -237,11 +299,13 @@ def main():
         slots.append(r)
 
     stats = {"masked": 0, "unmasked": 0, "F": 0.0, "B": 0.0, "refresh_reqs": 0, "rows": 0,
-             "cls": {}}
+             "cls": {}, "per_step": [], "req_steps": []}
 
     def one_step(account):
         for b in range(B):
             if slots[b].done:
+                if account:
+                    stats["req_steps"].append((slots[b].steps, slots[b].gen_len))
                 eng.release(slots[b])
                 slots[b] = make(b)
                 eng.admit(slots[b], cfg.mask_id)
@@ -249,8 +313,19 @@ def main():
         m = sum(r.masked_in_block for r in slots)
         refresh = sum(1 for r in slots
                       if w.cache_mode == "none" or r.refreshed_block != r.block_start)
-        counts = eng.step(slots)
+        ts = time.perf_counter()
+        counts = eng.step(slots)          # ends with the read-back of the counts
+        dt = time.perf_counter() - ts
         if account:
+            if w.cache_mode == "none":
+                kind = "no-cache"
+            elif refresh == 0:
+                kind = "cache"
+            elif refresh == len(slots):
+                kind = "refresh"
+            else:
+                kind = "mixed"
+            stats["per_step"].append((kind, dt, sum(n for n, _ in rows), refresh))
             stats["masked"] += m
             stats["unmasked"] += sum(counts)
             stats["refresh_reqs"] += refresh
@@ -338,6 +413,17 @@ def main():
             cpu["sample"] += ("; one request's no-cache step (the timed GPU steps batch "
                               f"{B} requests, cache mode {w.cache_mode})")
 
+    lat, dist = step_breakdown(stats["per_step"])
+    rs = stats["req_steps"]
+    req = ({"completed": len(rs), "mean_steps": sum(x[0] for x in rs) / len(rs),
+            "mean_tokens_per_step": sum(x[1] for x in rs) / sum(x[0] for x in rs)}
+           if rs else {"completed": 0})
+    if ceilings is not None:
+        ceilings["step_frac_of_measured_mfma"] = Fs / t_step / 1e12 / ceilings["mfma_bf16_tflops"]
+        if roof is not None:
+            ceilings["dominant_frac_of_measured"] = roof["achieved"] / (
+                ceilings["mfma_bf16_tflops"] if roof["unit"] == "TFLOP/s" else ceilings["copy_gbs"])
+
     out = {
         "metric": "denoise steps/s + unmasked tokens/s per MI355X; % MFMA / HBM roofline",
         "value": args.steps / elapsed,
@@ -361,6 +447,10 @@ def main():
                    "avg_refresh_requests": stats["refresh_reqs"] / args.steps},
         "roofline": roof,
         "step_roofline": step_roof,
+        "step_latency": lat,
+        "step_distribution": dist,
+        "requests": req,
+        "ceilings": ceilings,
         "kernels_profiled": kernels,
         "cpu_baseline": cpu,
     }

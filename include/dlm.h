@@ -201,6 +201,19 @@ typedef struct dlm_profile_entry {
 dlm_status dlm_profile_enable(dlm_model* m, int32_t on, const char* only_class);
 dlm_status dlm_profile_read(dlm_model* m, dlm_profile_entry* out, int32_t cap, int32_t* n_out);
 
+/* Measured ceilings (benchmark support, not part of the method). */
+/* dlm_ceiling_mfma: n_blocks blocks of 4 waves, each wave running iters x 32
+ * v_mfma_f32_16x16x32_bf16 over 8 independent accumulators; writes one float per wave to out
+ * (device, [4 n_blocks]) and the FLOPs executed to *flop_out (host, may be
+ * NULL). The caller times it on the stream. DLM_EINVAL for non-positive
+ * sizes or a NULL out. */
+dlm_status dlm_ceiling_mfma(int32_t n_blocks, int32_t iters, float* out, double* flop_out,
+                            void* stream);
+/* dlm_ceiling_copy: dst[0 .. bytes) = src[0 .. bytes) on the device with
+ * 16-byte vector loads and stores (bytes moved through HBM: 2 x bytes).
+ * Both pointers 16-byte aligned, bytes a multiple of 16, else DLM_EINVAL. */
+dlm_status dlm_ceiling_copy(const void* src, void* dst, size_t bytes, void* stream);
+
 /* Message for the last non-OK status on this thread ("" if none). */
 const char* dlm_last_error(void);
 

@@ -15,7 +15,7 @@ SRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libdlm.so")
 BUILD = os.path.join(os.path.dirname(PKG), "_build", "dlm")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["runtime.hip", "gemm.hip", "gemm_dl.hip", "rowwise.hip", "attention.hip"]
+SOURCES = ["runtime.hip", "gemm.hip", "gemm_dl.hip", "rowwise.hip", "attention.hip", "ceiling.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wno-unused-result"]

@@ -125,13 +125,14 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(
     if (kt + 1 < nkt) sstore(cur ^ 1);
     __syncthreads();
   }
-  epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM);
+  epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, (int)blockIdx.x,
+      (int)blockIdx.z);
 }
 
 // --------------------------------------------------------------- launch --
 template <class Epi>
 hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
-                          int K, int splits, const Epi& epi, hipStream_t st);
+                          int K, int splits, int group_m, const Epi& epi, hipStream_t st);
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads);
 
 // Register-staged kernel: any K that is a multiple of 16 bytes, fp32 or bf16.
@@ -163,7 +164,8 @@ template <typename T, class Epi>
 static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
                          int N, int K, const Epi& epi, hipStream_t st) {
   if constexpr (sizeof(T) == 2) {
-    if (p.cfg >= 0) return gemm_dl_launch<Epi>(p.cfg, A, lda, B, ldb, M, N, K, p.splits, epi, st);
+    if (p.cfg >= 0)
+      return gemm_dl_launch<Epi>(p.cfg, A, lda, B, ldb, M, N, K, p.splits, p.group_m, epi, st);
   }
   return launch_rs<T, Epi>(A, lda, B, ldb, M, N, K, p.splits, epi, st);
 }
@@ -176,8 +178,9 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // CU is latency-bound). Estimate = rounds x t_round x (K slice / 4096), plus
 // the HBM traffic of the fp32 K slices when K is split (written by the GEMM,
 // read back by the consumer); the cheapest (configuration, split) wins.
+// group_m selects the tile order (see gemm_dl_kernel).
 GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
-  GemmPlan best{-1, 1};
+  GemmPlan best{-1, 1, 0};
   if (M <= 0 || N <= 0) return best;
   if (es != 2 || K % 64 != 0) {
     if (splittable) {
@@ -213,10 +216,16 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
       if (s > 1) t += (double)M * N * 4.0 * 2.0 * (s - 1) / 5.0e12 * 1e6;
       if (t < best_t * 0.999) {
         best_t = t;
-        best = GemmPlan{c.cfg, s};
+        best = GemmPlan{c.cfg, s, 0};
       }
     }
   }
+  // weights larger than the last-level cache (256 MB Infinity Cache) stream
+  // from HBM once per row tile in plain order: use the grouped XCD order
+  int bm, bn, th;
+  if (best.cfg >= 0 && gemm_dl_tile(best.cfg, &bm, &bn, &th) && ceil_div(M, bm) > 1 &&
+      (double)N * K * es > 256e6)
+    best.group_m = 16;
   return best;
 }
 

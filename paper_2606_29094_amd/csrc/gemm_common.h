@@ -29,7 +29,10 @@ constexpr int kLdsRow = kRowBytes + 16; // padded LDS row stride
 
 // ------------------------------------------------------------ epilogues --
 // Each epilogue sees the wave's accumulators: acc[fm][fn][i] is the value at
-// row m0 + fm*16 + 4*(lane/16) + i, column n0 + fn*16 + lane%16.
+// row m0 + fm*16 + 4*(lane/16) + i, column n0 + fn*16 + lane%16. The further
+// arguments: wave column index, LDS scratch, waves per row, block rows, the
+// block's first row, its column-tile index and its K-split index (the kernel's
+// tile order decides these, not blockIdx).
 
 struct EpiStore {
   float* C; int ldc; long split_stride; int M, N;
@@ -37,8 +40,8 @@ struct EpiStore {
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
-    float* Cz = C + (long)blockIdx.z * split_stride;
+                             char*, int, int, int, int, int split) const {
+    float* Cz = C + (long)split * split_stride;
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -60,7 +63,7 @@ struct EpiScaledStore {
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
+                             char*, int, int, int, int, int) const {
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -82,7 +85,7 @@ struct EpiAdd {
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
+                             char*, int, int, int, int, int) const {
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -111,7 +114,7 @@ struct EpiSwiGLU {
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
-                             char*, int, int) const {
+                             char*, int, int, int, int, int) const {
     static_assert(FN % 2 == 0, "gate/up pairs");
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
@@ -155,7 +158,8 @@ struct EpiLMHead {
   __device__ bool skip_tile(int m0) const { return m_count && m0 >= *m_count; }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int wave_n,
-                             char* smem, int waves_n, int bm) const {
+                             char* smem, int waves_n, int bm, int block_m0,
+                             int tile_n, int) const {
     // stats per (fm, i) row for this lane over its FN columns
     RowStat st[FM][4];
 #pragma unroll
@@ -185,7 +189,7 @@ struct EpiLMHead {
       }
     // across the waves that share these rows (different column ranges): LDS
     RowStat* buf = reinterpret_cast<RowStat*>(smem);
-    const int wave_m_row0 = m0 - blockIdx.y * bm;  // wave's row offset inside the block tile
+    const int wave_m_row0 = m0 - block_m0;  // wave's row offset inside the block tile
     __syncthreads();
     if ((lane & 15) == 0) {
 #pragma unroll
@@ -197,9 +201,9 @@ struct EpiLMHead {
         }
     }
     __syncthreads();
-    const int tile = blockIdx.x;
+    const int tile = tile_n;
     for (int r = threadIdx.x; r < bm; r += blockDim.x) {
-      int m = blockIdx.y * bm + r;
+      int m = block_m0 + r;
       if (m >= M) continue;
       RowStat acc_r = buf[r * waves_n];
       for (int w = 1; w < waves_n; ++w) acc_r = combine(acc_r, buf[r * waves_n + w]);

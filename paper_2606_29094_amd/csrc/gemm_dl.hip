@@ -24,10 +24,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 typedef __attribute__((address_space(1))) const void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
 
+constexpr int kXcds = 8;      // XCDs the dispatcher spreads blocks over
+
 template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int RB, class Epi>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
-    int K, int k_per_split, Epi epi) {
+    int K, int k_per_split, int group_m, Epi epi) {
   static_assert(RB == 64 || RB == 128, "k-tile row bytes");
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
@@ -46,9 +48,37 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  // Tile order. group_m == 0: block (x, y, z) = (column tile, row tile,
+  // K slice). group_m > 0 (weight matrices larger than the last-level cache):
+  // the dispatcher hands out blocks in linear order (x fastest, then y, then
+  // z) round-robin over the 8 XCDs (block i to XCD i mod 8), each with its
+  // own L2. The linear id is remapped so that each XCD receives one contiguous
+  // range of a logical order that goes down a group of group_m row tiles
+  // before moving to the next column tile: blocks sharing a weight column
+  // tile run on the same XCD at about the same time, and each column tile is
+  // fetched from HBM about once per group of row tiles instead of once per
+  // row tile.
+  int tm = blockIdx.y, tn = blockIdx.x, tz = blockIdx.z;
+  if (group_m > 0) {
+    const int n_n = gridDim.x, n_m = gridDim.y;
+    const int plane = n_n * n_m;
+    const int total = plane * gridDim.z;
+    const int id = (blockIdx.z * n_m + blockIdx.y) * n_n + blockIdx.x;
+    const int xcd = id % kXcds, per = total / kXcds, rem = total % kXcds;
+    const int lid = xcd * per + min(xcd, rem) + id / kXcds;
+    tz = lid / plane;
+    const int l = lid - tz * plane;
+    const int per_group = group_m * n_n;
+    const int gi = l / per_group;
+    const int first = gi * group_m;
+    const int gsz = min(n_m - first, group_m);
+    const int r = l - gi * per_group;
+    tm = first + r % gsz;
+    tn = r / gsz;
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
   if (epi.skip_tile(m0)) return;   // uniform over the block
-  const int kbeg = blockIdx.z * k_per_split;
+  const int kbeg = tz * k_per_split;
   const int kend = min(K, kbeg + k_per_split);
   const int nkt = kend > kbeg ? (kend - kbeg) / BK : 0;
 
@@ -142,7 +172,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     compute(kt % STAGES);
   }
   __syncthreads();
-  epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM);
+  epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
 }
 
 // Tile configurations (BM, BN, waves M x N, stages, k-tile row bytes).
@@ -173,7 +203,7 @@ int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
 
 template <class Epi>
 hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
-                          int K, int splits, const Epi& epi, hipStream_t st) {
+                          int K, int splits, int group_m, const Epi& epi, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (K % 64 != 0 || splits < 1 || (K / 64) % splits != 0) return hipErrorInvalidValue;
   const int kps = K / splits;
@@ -183,7 +213,7 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
     dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                  \
     hipLaunchKernelGGL((gemm_dl_kernel<BM_, BN_, WM_, WN_, S_, RB_, Epi>), g,             \
                        dim3(WM_ * WN_ * 64),                                             \
-                       0, st, A, lda, B, ldb, M, N, K, kps, epi);                        \
+                       0, st, A, lda, B, ldb, M, N, K, kps, group_m, epi);                        \
     return hipGetLastError();                                                            \
   }
     DL_CONFIGS(X)
@@ -193,16 +223,16 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
 }
 
 template hipError_t gemm_dl_launch<EpiStore>(int, const bf16*, int, const bf16*, int, int, int,
-                                             int, int, const EpiStore&, hipStream_t);
+                                             int, int, int, const EpiStore&, hipStream_t);
 template hipError_t gemm_dl_launch<EpiAdd>(int, const bf16*, int, const bf16*, int, int, int,
-                                           int, int, const EpiAdd&, hipStream_t);
+                                           int, int, int, const EpiAdd&, hipStream_t);
 template hipError_t gemm_dl_launch<EpiScaledStore>(int, const bf16*, int, const bf16*, int, int,
-                                                   int, int, int, const EpiScaledStore&,
+                                                   int, int, int, int, const EpiScaledStore&,
                                                    hipStream_t);
 template hipError_t gemm_dl_launch<EpiSwiGLU<bf16>>(int, const bf16*, int, const bf16*, int, int,
-                                                    int, int, int, const EpiSwiGLU<bf16>&,
+                                                    int, int, int, int, const EpiSwiGLU<bf16>&,
                                                     hipStream_t);
 template hipError_t gemm_dl_launch<EpiLMHead>(int, const bf16*, int, const bf16*, int, int, int,
-                                              int, int, const EpiLMHead&, hipStream_t);
+                                              int, int, int, const EpiLMHead&, hipStream_t);
 
 }  // namespace dlm

@@ -47,7 +47,7 @@ __device__ __forceinline__ int plan_req_of_tile(const StepPlan& p, int tile) {
 // ---- GEMM family (gemm.hip, gemm_dl.hip) ----
 // cfg >= 0: a direct-load tile configuration (bf16); cfg < 0: register-staged
 // kernel. splits: number of K slices (fp32 partial slices, summed by the consumer).
-struct GemmPlan { int cfg; int splits; };
+struct GemmPlan { int cfg; int splits; int group_m; };   // group_m: tile order (0 = plain)
 GemmPlan gemm_plan(int elem_bytes, int M, int N, int K, bool splittable, int num_cu);
 template <typename T>
 hipError_t gemm_store_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,

@@ -25,7 +25,7 @@ EXPORTS = ["dlm_load_weights", "dlm_model_destroy", "dlm_workspace_bytes",
            "dlm_kv_cache_alloc", "dlm_cache_destroy", "dlm_cache_invalidate",
            "dlm_denoise_step", "dlm_cache_refresh", "dlm_debug_logits",
            "dlm_head_confidence", "dlm_profile_enable", "dlm_profile_read",
-           "dlm_last_error"]
+           "dlm_ceiling_mfma", "dlm_ceiling_copy", "dlm_last_error"]
 
 
 class DlmConfig(ctypes.Structure):
@@ -101,6 +101,9 @@ def lib():
         L.dlm_profile_enable.argtypes = [c_void_p, c_int32, ctypes.c_char_p]
         L.dlm_profile_read.argtypes = [c_void_p, POINTER(DlmProfileEntry), c_int32,
                                        POINTER(c_int32)]
+        L.dlm_ceiling_mfma.argtypes = [c_int32, c_int32, c_void_p, POINTER(ctypes.c_double),
+                                       c_void_p]
+        L.dlm_ceiling_copy.argtypes = [c_void_p, c_void_p, c_size_t, c_void_p]
         L.dlm_last_error.argtypes = []
         L.dlm_last_error.restype = ctypes.c_char_p
         for name in ["dlm_load_weights", "dlm_workspace_bytes", "dlm_kv_cache_alloc",
@@ -217,3 +220,15 @@ def profile_read(model, cap: int = 64) -> dict:
     n = c_int32()
     check(lib().dlm_profile_read(model, arr, cap, ctypes.byref(n)))
     return {arr[i].name.decode(): (arr[i].calls, arr[i].total_ms) for i in range(n.value)}
+
+
+def ceiling_mfma(n_blocks: int, iters: int, out_ptr: int, stream: int) -> float:
+    """Enqueue the bf16 MFMA loop; returns the FLOPs it executes."""
+    f = ctypes.c_double()
+    check(lib().dlm_ceiling_mfma(n_blocks, iters, out_ptr, ctypes.byref(f), stream))
+    return f.value
+
+
+def ceiling_copy(src_ptr: int, dst_ptr: int, nbytes: int, stream: int) -> None:
+    """Enqueue a device copy of nbytes (16-byte aligned, multiple of 16)."""
+    check(lib().dlm_ceiling_copy(src_ptr, dst_ptr, nbytes, stream))
