@@ -233,6 +233,8 @@ def main():
                          "(per-class breakdown, choice of the dominant kernel)")
     ap.add_argument("--no-profile", action="store_true",
                     help="time without the per-kernel event records")
+    ap.add_argument("--stats", action="store_true",
+                    help="also compute the per-request confidence statistics in every step")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-loop and copy ceilings")
     args = ap.parse_args()
@@ -291,7 +293,7 @@ def main():
         max_len = w.prompt_range[1] + max(w.gen_choices)
     else:
         max_len = w.prompt_len + w.gen_len
-    eng = engine.Engine(model, B, max_len, w.cache_mode, max_rows=B * max_len)
+    eng = engine.Engine(model, B, max_len, w.cache_mode, max_rows=B * max_len, stats=args.stats)
     slots = []
     for b in range(B):
         r = make(b)
@@ -444,7 +446,8 @@ def main():
                    "weights": "synthetic N(0,0.02) seed 0",
                    "avg_recomputed_rows": stats["rows"] / args.steps,
                    "avg_masked_rows": stats["masked"] / args.steps,
-                   "avg_refresh_requests": stats["refresh_reqs"] / args.steps},
+                   "avg_refresh_requests": stats["refresh_reqs"] / args.steps,
+                   "confidence_stats": bool(args.stats)},
         "roofline": roof,
         "step_roofline": step_roof,
         "step_latency": lat,

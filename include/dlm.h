@@ -65,7 +65,8 @@ typedef enum {
 enum {
   DLM_MAX_BLOCK = 64,     /* largest block length (one 64-lane wavefront per request) */
   DLM_MAX_REQ = 64,       /* largest number of requests in one step                     */
-  DLM_MAX_SEQ = 8192      /* largest sequence length                                    */
+  DLM_MAX_SEQ = 8192,     /* largest sequence length                                    */
+  DLM_NSTATS = 8          /* confidence statistics per request (dlm_step_out.stats)    */
 };
 
 /* Request flag: this step is a recompute step (whole sequence, cache rewritten). */
@@ -116,6 +117,10 @@ typedef struct dlm_batch {
   int32_t* tokens;        /* device, packed token ids; updated in place                  */
   uint8_t* mask;          /* device, packed, 1 = [MASK]; updated in place                */
   int32_t mode;           /* dlm_cache_mode                                              */
+  float* tok_conf;        /* optional device, packed like tokens: the confidence with which
+                             each position was unmasked. The step writes it for every
+                             position it unmasks; positions the caller unmasks itself hold
+                             what the caller wrote. Required when dlm_step_out.stats is set. */
 } dlm_batch;
 
 /* Step outputs (device). Request r's entries start at r * DLM_MAX_BLOCK. */
@@ -128,6 +133,17 @@ typedef struct dlm_step_out {
                              position masked at step start (index = pos - block_start),
                              -1 for positions that were already unmasked                  */
   int32_t* block_tok;     /* optional, same layout: prediction of each masked position   */
+  float* stats;           /* optional [n_req * DLM_NSTATS], after this step's unmasking:
+                             the Step Predictor's confidence features (paper, "Step
+                             Prediction" and the appendix "Step Predictor Features") over
+                             the request's output tokens, i.e. the unmasked positions of
+                             [prompt_len, seq_len), each valued at batch.tok_conf:
+                             [0] count n, [1] min, [2] lower quartile, [3] median, [4] mean,
+                             [5] upper quartile, [6] max, [7] unmasked positions of the
+                             active block. Quartiles and median interpolate linearly
+                             between order statistics (p-quantile of the ascending v:
+                             v[j] + (h - j)(v[j+1] - v[j]), h = (n-1)p, j = floor(h)).
+                             With n = 0, [1..6] are 0. fp32; the mean is a fixed-order sum. */
 } dlm_step_out;
 
 typedef struct dlm_model dlm_model;

@@ -8,6 +8,7 @@ namespace dlm {
 
 constexpr int kMaxReq = 64;
 constexpr int kMaxBlock = 64;
+constexpr int kNStats = 8;      // confidence statistics per request
 constexpr int kQTile = 64;      // query rows per attention block / rows per RoPE tile
 
 // Per-request plan of one step, passed by value as a kernel argument.
@@ -16,6 +17,7 @@ struct ReqPlan {
   int nrows;     // recompute rows
   int pos0;      // position of the first recompute row
   int seq_len;   // keys attended (all positions of the slot)
+  int prompt_len;
   int slot;
   int tok_off;   // offset of position 0 in tokens/mask
   int blk_s;     // active block [blk_s, blk_s + blk_len)
@@ -94,7 +96,8 @@ hipError_t lm_combine(const float* pm, const float* ps, const int* pi, int tiles
 hipError_t unmask_select(const StepPlan& p, const float* conf, const int* tok,
                          const int* req_lm_off, int32_t* tokens, uint8_t* mask,
                          int32_t* n_unmasked, int32_t* out_pos, int32_t* out_tok,
-                         float* out_conf, float* blk_conf, int32_t* blk_tok, hipStream_t st);
+                         float* out_conf, float* blk_conf, int32_t* blk_tok, float* tok_conf,
+                         float* stats, hipStream_t st);
 
 // ---- attention (attention.hip) ----
 template <typename T>

@@ -341,63 +341,150 @@ hipError_t lm_combine(const float* pm, const float* ps, const int* pi, int tiles
 }
 
 // -------------------------------------------------- threshold / unmask --
-// One wave per request, lane j = block position blk_s + j. Masked positions
-// whose confidence exceeds gamma are unmasked; if none does, the most
-// confident masked position (lowest position on ties) is unmasked alone.
+// Wave 0 of the request's block, lane j = block position blk_s + j. Masked
+// positions whose confidence exceeds gamma are unmasked; if none does, the
+// most confident masked position (lowest position on ties) is unmasked alone.
 // Unmasked (pos, tok, conf) are written in ascending position order.
-__global__ __launch_bounds__(64) void unmask_kernel(
+// Optional statistics (paper, "Step Prediction"; appendix "Step Predictor
+// Features"): count, min, quartiles, median, mean and max of the confidences of
+// the request's unmasked output positions, and the unmasked count of the block.
+constexpr int kUnmaskThreads = 256;
+constexpr int kStatCap = 8192;          // largest sequence length: output positions per request
+
+// One block per request. Wave 0 takes the unmask decision over the active
+// block (one lane per position); with stats requested, the whole block then
+// gathers the confidences of the request's unmasked output positions into
+// LDS (order does not matter: they are sorted next), sorts them with a
+// bitonic network and reads the order statistics off the sorted array.
+__global__ __launch_bounds__(kUnmaskThreads) void unmask_kernel(
     StepPlan p, const float* __restrict__ conf, const int* __restrict__ tok,
     const int* __restrict__ req_lm_off, int32_t* __restrict__ tokens, uint8_t* __restrict__ mask,
     int32_t* __restrict__ n_unmasked, int32_t* __restrict__ out_pos, int32_t* __restrict__ out_tok,
-    float* __restrict__ out_conf, float* __restrict__ blk_conf, int32_t* __restrict__ blk_tok) {
+    float* __restrict__ out_conf, float* __restrict__ blk_conf, int32_t* __restrict__ blk_tok,
+    float* __restrict__ tok_conf, float* __restrict__ stats) {
   const int r = blockIdx.x;
   const ReqPlan& q = p.r[r];
-  const int lane = threadIdx.x;
-  const long ti = (long)q.tok_off + q.blk_s + lane;
-  const bool in_blk = lane < q.blk_len;
-  const bool masked = in_blk && mask[ti] != 0;
-  const unsigned long long mb = __ballot(masked);
-  float c = -1.0f;
-  int t = 0;
-  if (masked) {
-    const int idx = req_lm_off[r] + __popcll(mb & ((1ull << lane) - 1ull));
-    c = conf[idx];
-    t = tok[idx];
-  }
-  bool sel = masked && c > q.gamma;
-  unsigned long long sb = __ballot(sel);
-  if (sb == 0ull && mb != 0ull) {
-    // wave argmax of c over masked lanes, lowest lane on ties
-    float bc = masked ? c : -2.0f;
-    int bl = masked ? lane : 64;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      float oc = __shfl_xor(bc, o, 64);
-      int ol = __shfl_xor(bl, o, 64);
-      if (oc > bc || (oc == bc && ol < bl)) { bc = oc; bl = ol; }
+  const int tid = threadIdx.x;
+  if (tid < 64) {
+    const int lane = tid;
+    const long ti = (long)q.tok_off + q.blk_s + lane;
+    const bool in_blk = lane < q.blk_len;
+    const bool masked = in_blk && mask[ti] != 0;
+    const unsigned long long mb = __ballot(masked);
+    float c = -1.0f;
+    int t = 0;
+    if (masked) {
+      const int idx = req_lm_off[r] + __popcll(mb & ((1ull << lane) - 1ull));
+      c = conf[idx];
+      t = tok[idx];
     }
-    sel = lane == bl;
-    sb = __ballot(sel);
+    bool sel = masked && c > q.gamma;
+    unsigned long long sb = __ballot(sel);
+    if (sb == 0ull && mb != 0ull) {
+      // wave argmax of c over masked lanes, lowest lane on ties
+      float bc = masked ? c : -2.0f;
+      int bl = masked ? lane : 64;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        float oc = __shfl_xor(bc, o, 64);
+        int ol = __shfl_xor(bl, o, 64);
+        if (oc > bc || (oc == bc && ol < bl)) { bc = oc; bl = ol; }
+      }
+      sel = lane == bl;
+      sb = __ballot(sel);
+    }
+    if (blk_conf) blk_conf[r * kMaxBlock + lane] = masked ? c : -1.0f;
+    if (blk_tok) blk_tok[r * kMaxBlock + lane] = masked ? t : -1;
+    if (sel) {
+      const int k = __popcll(sb & ((1ull << lane) - 1ull));
+      out_pos[r * kMaxBlock + k] = q.blk_s + lane;
+      out_tok[r * kMaxBlock + k] = t;
+      out_conf[r * kMaxBlock + k] = c;
+      tokens[ti] = t;
+      mask[ti] = 0;
+      if (tok_conf) tok_conf[ti] = c;
+    }
+    if (lane == 0) {
+      n_unmasked[r] = __popcll(sb);
+      if (stats) stats[r * kNStats + 7] = (float)(q.blk_len - __popcll(mb) + __popcll(sb));
+    }
   }
-  if (blk_conf) blk_conf[r * kMaxBlock + lane] = masked ? c : -1.0f;
-  if (blk_tok) blk_tok[r * kMaxBlock + lane] = masked ? t : -1;
-  if (sel) {
-    const int k = __popcll(sb & ((1ull << lane) - 1ull));
-    out_pos[r * kMaxBlock + k] = q.blk_s + lane;
-    out_tok[r * kMaxBlock + k] = t;
-    out_conf[r * kMaxBlock + k] = c;
-    tokens[ti] = t;
-    mask[ti] = 0;
+  if (!stats) return;                         // uniform: a kernel argument
+  __shared__ float sv[kStatCap];
+  __shared__ int s_n;
+  __shared__ float s_part[kUnmaskThreads / 64];
+  if (tid == 0) s_n = 0;
+  __syncthreads();                            // also publishes wave 0's mask / tok_conf writes
+  // gather (LDS atomic slot: the order is irrelevant, the values are sorted)
+  const long base = q.tok_off;
+  for (int pos = q.prompt_len + tid; pos < q.seq_len; pos += kUnmaskThreads) {
+    if (mask[base + pos] == 0) {
+      const float v = tok_conf[base + pos];
+      sv[atomicAdd(&s_n, 1)] = v;
+    }
   }
-  if (lane == 0) n_unmasked[r] = __popcll(sb);
+  __syncthreads();
+  const int n = s_n;
+  int n2 = 1;
+  while (n2 < n) n2 <<= 1;
+  for (int i = n + tid; i < n2; i += kUnmaskThreads) sv[i] = INFINITY;
+  __syncthreads();
+  // bitonic sort, ascending
+  for (int k = 2; k <= n2; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < n2; i += kUnmaskThreads) {
+        const int ij = i ^ j;
+        if (ij > i) {
+          const float a = sv[i], b = sv[ij];
+          if ((a > b) == ((i & k) == 0)) {
+            sv[i] = b;
+            sv[ij] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // mean over the sorted array (the gather order depends on scheduling):
+  // per-thread strided sums, then a fixed-order reduction
+  float lsum = 0.f;
+  for (int i = tid; i < n; i += kUnmaskThreads) lsum += sv[i];
+  lsum = wave_sum(lsum);
+  if ((tid & 63) == 0) s_part[tid >> 6] = lsum;
+  __syncthreads();
+  if (tid == 0) {
+    float* o = stats + r * kNStats;
+    o[0] = (float)n;
+    if (n == 0) {
+      for (int i = 1; i < 7; ++i) o[i] = 0.f;
+    } else {
+      float tot = 0.f;
+      for (int w = 0; w < kUnmaskThreads / 64; ++w) tot += s_part[w];
+      auto quant = [&](int quarter) {     // p = quarter / 4: h = (n-1) p is exact in fp32
+        const int hq = (n - 1) * quarter;
+        const int j = hq / 4;
+        const float f = (float)(hq % 4) * 0.25f;
+        const float lo = sv[j], hi = j + 1 < n ? sv[j + 1] : sv[j];
+        return fmaf(f, hi - lo, lo);
+      };
+      o[1] = sv[0];
+      o[2] = quant(1);
+      o[3] = quant(2);
+      o[4] = tot / (float)n;
+      o[5] = quant(3);
+      o[6] = sv[n - 1];
+    }
+  }
 }
 
 hipError_t unmask_select(const StepPlan& p, const float* conf, const int* tok,
                          const int* req_lm_off, int32_t* tokens, uint8_t* mask,
                          int32_t* n_unmasked, int32_t* out_pos, int32_t* out_tok,
-                         float* out_conf, float* blk_conf, int32_t* blk_tok, hipStream_t st) {
-  hipLaunchKernelGGL(unmask_kernel, dim3(p.n_req), dim3(64), 0, st, p, conf, tok, req_lm_off,
-                     tokens, mask, n_unmasked, out_pos, out_tok, out_conf, blk_conf, blk_tok);
+                         float* out_conf, float* blk_conf, int32_t* blk_tok, float* tok_conf,
+                         float* stats, hipStream_t st) {
+  hipLaunchKernelGGL(unmask_kernel, dim3(p.n_req), dim3(kUnmaskThreads), 0, st, p, conf, tok,
+                     req_lm_off, tokens, mask, n_unmasked, out_pos, out_tok, out_conf, blk_conf,
+                     blk_tok, tok_conf, stats);
   return hipGetLastError();
 }
 

@@ -253,6 +253,7 @@ dlm_status make_plan(const dlm_model* m, const dlm_cache* c, const dlm_batch* b,
     rp.nrows = r1 - r0;
     rp.pos0 = r0;
     rp.seq_len = q.seq_len;
+    rp.prompt_len = q.prompt_len;
     rp.slot = q.slot;
     rp.tok_off = q.tok_offset;
     rp.blk_s = q.block_start;
@@ -375,7 +376,8 @@ dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPl
                            cf.inv_tau, pm, ps, pi, L.m_max, lm_count, st));
   LAUNCH(m, st, "lm_combine", lm_combine(pm, ps, pi, L.tiles, L.m_max, lm_count, m_max, conf, tok, st));
   LAUNCH(m, st, "unmask", unmask_select(p, conf, tok, req_off, b->tokens, b->mask, out->n_unmasked, out->pos,
-                         out->tok, out->conf, out->block_conf, out->block_tok, st));
+                         out->tok, out->conf, out->block_conf, out->block_tok, b->tok_conf,
+                         out->stats, st));
   return DLM_OK;
 }
 
@@ -556,6 +558,8 @@ dlm_status dlm_denoise_step(dlm_model* m, dlm_cache* c, const dlm_batch* b,
   if (!thresholds) return fail(DLM_EINVAL, "thresholds is NULL");
   if (!out || !out->n_unmasked || !out->pos || !out->tok || !out->conf)
     return fail(DLM_EINVAL, "step output pointer is NULL");
+  if (out->stats && (!b || !b->tok_conf))
+    return fail(DLM_EINVAL, "confidence statistics need batch.tok_conf");
   StepPlan p;
   s = make_plan(m, c, b, thresholds, false, &p);
   if (s != DLM_OK) return s;

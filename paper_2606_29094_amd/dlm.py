@@ -18,6 +18,7 @@ DLM_OK, DLM_EINVAL, DLM_ESIZE, DLM_EHIP, DLM_ESTATE, DLM_EUNSUPPORTED = 0, -1, -
 DLM_F32, DLM_BF16 = 0, 1
 DLM_CACHE_NONE, DLM_CACHE_PREFIX, DLM_CACHE_DUAL = 0, 1, 2
 DLM_MAX_BLOCK, DLM_MAX_REQ, DLM_MAX_SEQ = 64, 64, 8192
+DLM_NSTATS = 8
 DLM_REQ_REFRESH = 1
 MODES = {"none": DLM_CACHE_NONE, "prefix": DLM_CACHE_PREFIX, "dual": DLM_CACHE_DUAL}
 
@@ -53,12 +54,13 @@ class DlmReq(ctypes.Structure):
 
 class DlmBatch(ctypes.Structure):
     _fields_ = [("n_req", c_int32), ("reqs", POINTER(DlmReq)), ("tokens", c_void_p),
-                ("mask", c_void_p), ("mode", c_int32)]
+                ("mask", c_void_p), ("mode", c_int32), ("tok_conf", c_void_p)]
 
 
 class DlmStepOut(ctypes.Structure):
     _fields_ = [("n_unmasked", c_void_p), ("pos", c_void_p), ("tok", c_void_p),
-                ("conf", c_void_p), ("block_conf", c_void_p), ("block_tok", c_void_p)]
+                ("conf", c_void_p), ("block_conf", c_void_p), ("block_tok", c_void_p),
+                ("stats", c_void_p)]
 
 
 class DlmProfileEntry(ctypes.Structure):
@@ -169,18 +171,19 @@ def cache_invalidate(cache, slot: int):
     check(lib().dlm_cache_invalidate(cache, slot))
 
 
-def make_batch(reqs, tokens, mask, mode: int):
+def make_batch(reqs, tokens, mask, mode: int, tok_conf=None):
     arr = (DlmReq * len(reqs))(*reqs)
     b = DlmBatch(len(reqs), ctypes.cast(arr, POINTER(DlmReq)), tokens.data_ptr(),
-                 mask.data_ptr(), mode)
+                 mask.data_ptr(), mode, None if tok_conf is None else tok_conf.data_ptr())
     b._keep = arr
     return b
 
 
-def make_step_out(n_unmasked, pos, tok, conf, block_conf=None, block_tok=None):
+def make_step_out(n_unmasked, pos, tok, conf, block_conf=None, block_tok=None, stats=None):
     return DlmStepOut(n_unmasked.data_ptr(), pos.data_ptr(), tok.data_ptr(), conf.data_ptr(),
                       None if block_conf is None else block_conf.data_ptr(),
-                      None if block_tok is None else block_tok.data_ptr())
+                      None if block_tok is None else block_tok.data_ptr(),
+                      None if stats is None else stats.data_ptr())
 
 
 def denoise_step(model, cache, batch: DlmBatch, thresholds, out: DlmStepOut, workspace,

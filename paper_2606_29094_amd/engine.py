@@ -128,7 +128,7 @@ class Engine:
     """Slots, workspace and packed token/mask buffers for a fixed set of slots."""
 
     def __init__(self, model: DeviceModel, n_slots: int, max_seq_len: int, mode: str,
-                 max_rows: Optional[int] = None, device="cuda:0"):
+                 max_rows: Optional[int] = None, device="cuda:0", stats: bool = False):
         self.model = model
         self.mode = mode
         self.mode_id = dlm.MODES[mode]
@@ -146,6 +146,10 @@ class Engine:
         self.workspace = torch.empty(ws, dtype=torch.uint8, device=self.device)
         self.tokens = torch.zeros(n_slots * max_seq_len, dtype=torch.int32, device=self.device)
         self.mask = torch.zeros(n_slots * max_seq_len, dtype=torch.uint8, device=self.device)
+        # confidence each position was unmasked with, and the per-request
+        # statistics of those of the output tokens (Step Predictor features)
+        self.tok_conf = (torch.zeros(n_slots * max_seq_len, dtype=torch.float32,
+                                     device=self.device) if stats else None)
         R = n_slots
         B = dlm.DLM_MAX_BLOCK
         self.n_unmasked = torch.zeros(R, dtype=torch.int32, device=self.device)
@@ -154,9 +158,12 @@ class Engine:
         self.out_conf = torch.zeros(R * B, dtype=torch.float32, device=self.device)
         self.block_conf = torch.zeros(R * B, dtype=torch.float32, device=self.device)
         self.block_tok = torch.zeros(R * B, dtype=torch.int32, device=self.device)
+        self.stats = (torch.zeros(R * dlm.DLM_NSTATS, dtype=torch.float32, device=self.device)
+                      if stats else None)
         self.host_n = torch.zeros(R, dtype=torch.int32).pin_memory()
         self.step_out = dlm.make_step_out(self.n_unmasked, self.out_pos, self.out_tok,
-                                          self.out_conf, self.block_conf, self.block_tok)
+                                          self.out_conf, self.block_conf, self.block_tok,
+                                          self.stats)
         self.free_slots = list(range(n_slots))[::-1]
 
     def close(self):
@@ -185,11 +192,15 @@ class Engine:
         self.free_slots.append(req.slot)
         req.slot = -1
 
-    def set_state(self, req: Request, tokens: np.ndarray, mask: np.ndarray, k: int):
+    def set_state(self, req: Request, tokens: np.ndarray, mask: np.ndarray, k: int,
+                  tok_conf: Optional[np.ndarray] = None):
         """Overwrite a request's tokens/mask/block (teacher forcing in tests)."""
         o = req.tok_offset
         self.tokens[o:o + req.seq_len].copy_(torch.from_numpy(np.asarray(tokens, np.int32)))
         self.mask[o:o + req.seq_len].copy_(torch.from_numpy(np.asarray(mask, np.uint8)))
+        if tok_conf is not None:
+            self.tok_conf[o:o + req.seq_len].copy_(
+                torch.from_numpy(np.asarray(tok_conf, np.float32)))
         req.k = k
         if not req.done:
             s = req.block_start
@@ -207,7 +218,7 @@ class Engine:
 
     def enqueue_step(self, reqs: List[Request], stream=None):
         dreqs = self.dlm_reqs(reqs)
-        batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id)
+        batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id, self.tok_conf)
         dlm.denoise_step(self.model.handle, self.cache, batch, [r.threshold for r in reqs],
                          self.step_out, self.workspace, stream)
         for r, d in zip(reqs, dreqs):
@@ -261,7 +272,7 @@ class Engine:
 
     def read_outputs(self, n_req: int):
         B = dlm.DLM_MAX_BLOCK
-        return {
+        out = {
             "n": self.n_unmasked[:n_req].cpu().numpy(),
             "pos": self.out_pos[:n_req * B].view(n_req, B).cpu().numpy(),
             "tok": self.out_tok[:n_req * B].view(n_req, B).cpu().numpy(),
@@ -269,3 +280,10 @@ class Engine:
             "block_conf": self.block_conf[:n_req * B].view(n_req, B).cpu().numpy(),
             "block_tok": self.block_tok[:n_req * B].view(n_req, B).cpu().numpy(),
         }
+        if self.stats is not None:
+            out["stats"] = self.stats[:n_req * dlm.DLM_NSTATS].view(n_req, dlm.DLM_NSTATS).cpu().numpy()
+        return out
+
+    def read_tok_conf(self, req: Request) -> np.ndarray:
+        o = req.tok_offset
+        return self.tok_conf[o:o + req.seq_len].cpu().numpy()
