@@ -187,6 +187,48 @@ def measure_ceilings(torch, dlm):
                       "1 GiB device copy, 16-byte lanes (read + write bytes)"}
 
 
+def serve_main(args, w, cfg, inv_tau):
+    """Continuous batching of a Poisson trace on one GPU with the threshold
+    controller (latency profile and steps-per-block table measured earlier on
+    the same kind of GPU and committed under profiles/)."""
+    import synth
+    import synth.device as sdev
+    from paper_2606_29094_amd import engine, serving
+    from paper_2606_29094_amd.profiling import StepTable
+    ctl_file = os.path.join(ROOT, "profiles", "controller_mha8b.json")
+    meas = json.load(open(ctl_file))
+    table = StepTable.from_json(meas["step_table"])
+    gammas = table.gammas
+    if args.fixed_threshold is not None:
+        g = args.fixed_threshold
+        i = min(range(len(gammas)), key=lambda j: abs(gammas[j] - g))
+        table = StepTable([gammas[i]], [table.steps_per_block[i]], table.block)
+        gammas = [gammas[i]]
+    mcfg = synth.MHA_8B
+    t = sdev.model_tensors(mcfg)
+    model = engine.DeviceModel(engine.ModelShape.of(mcfg), t, inv_tau)
+    slots, prange, gens = 32, (128, 2048), (128, 256)
+    max_len = prange[1] + max(gens)
+    eng = engine.Engine(model, slots, max_len, "dual", max_rows=16384)
+    scfg = serving.ServeConfig(gammas, 32, "dual", max_step_tokens=16384)
+    srv = serving.Server(eng, scfg, meas["latency_profile"], table, mcfg.mask_id)
+    trace = serving.poisson_trace(args.serve, args.serve_requests, 7, prange, gens, args.slo,
+                                  mcfg.vocab)
+    # warm-up: a few requests outside the measured trace
+    warm = serving.poisson_trace(100.0, 4, 99, prange, gens, 1e9, mcfg.vocab)
+    serving.Server(eng, scfg, meas["latency_profile"], table, mcfg.mask_id).run(warm)
+    rep = srv.run(trace)
+    print(json.dumps({"metric": "serving: SLO attainment / tokens/s", "value": rep["slo_attainment"],
+                      "unit": "fraction of requests within SLO", "report": rep,
+                      "config": {"workload": "poisson-serve-mha8b-dual", "rate_per_s": args.serve,
+                                 "requests": args.serve_requests, "slo_s": args.slo,
+                                 "thresholds": gammas, "slots": slots,
+                                 "max_step_tokens": 16384, "prompt_range": list(prange),
+                                 "gen_choices": list(gens), "inv_tau": inv_tau,
+                                 "controller_measurements": os.path.relpath(ctl_file, ROOT)},
+                      "data": "synthetic"}), flush=True)
+
+
 def step_breakdown(per_step):
     """Per-step-type latency and the distributions of recomputed rows and
     refreshing requests over the timed steps."""
@@ -235,6 +277,17 @@ def main():
                     help="time without the per-kernel event records")
     ap.add_argument("--stats", action="store_true",
                     help="also compute the per-request confidence statistics in every step")
+    ap.add_argument("--latency-profile", action="store_true",
+                    help="only measure per-step latency over batch sizes in tokens (recompute "
+                         "and dual-cache steps) for the workload's model and print it")
+    ap.add_argument("--serve", type=float, default=None, metavar="RATE",
+                    help="run the single-GPU serving loop on a Poisson trace of RATE requests/s "
+                         "(heterogeneous MHA-8B requests, dual cache, controller thresholds) "
+                         "and print its report")
+    ap.add_argument("--serve-requests", type=int, default=200)
+    ap.add_argument("--slo", type=float, default=10.0, help="latency SLO of --serve (s)")
+    ap.add_argument("--fixed-threshold", type=float, default=None,
+                    help="--serve with this single threshold instead of the controller's choice")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-loop and copy ceilings")
     args = ap.parse_args()
@@ -270,6 +323,16 @@ def main():
         inv_tau, tau_src = args.inv_tau, "command line"
     else:
         inv_tau, tau_src = load_inv_tau(cfg.name)
+    if args.serve is not None:
+        serve_main(args, w, cfg, inv_tau)
+        return
+    if args.latency_profile:
+        from paper_2606_29094_amd import profiling
+        lp = profiling.latency_profile(cfg, inv_tau)
+        print(json.dumps({"metric": "per-step latency over batch size (tokens)",
+                          "unit": "s", "latency_profile": lp, "data": "synthetic",
+                          "config": {"workload": w.name, "inv_tau": inv_tau}}), flush=True)
+        return
     tensors = sdev.model_tensors(cfg)
     shape = engine.ModelShape.of(cfg)
     model = engine.DeviceModel(shape, tensors, inv_tau)

@@ -1,4 +1,5 @@
-"""Build libdlm.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Build libdlm.so (the HIP kernels and the C ABI) for gfx950 with hipcc, and
+libdlmctl.so (the host-only threshold controller) with g++.
 
 Usage: python -m paper_2606_29094_amd.build  (or call build()).
 Every call recompiles; objects go to _build/ next to the package.
@@ -13,6 +14,7 @@ from concurrent.futures import ThreadPoolExecutor
 PKG = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libdlm.so")
+CTL_OUT = os.path.join(PKG, "libdlmctl.so")
 BUILD = os.path.join(os.path.dirname(PKG), "_build", "dlm")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["runtime.hip", "gemm.hip", "gemm_dl.hip", "rowwise.hip", "attention.hip", "ceiling.hip"]
@@ -47,7 +49,16 @@ def build(verbose: bool = False) -> str:
     tmp = OUT + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, OUT)
+    build_controller()
     return OUT
+
+
+def build_controller() -> str:
+    tmp = CTL_OUT + ".tmp"
+    _run(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-Wall", "-Wextra", "-o", tmp,
+          os.path.join(SRC, "controller.cpp")])
+    os.replace(tmp, CTL_OUT)
+    return CTL_OUT
 
 
 if __name__ == "__main__":

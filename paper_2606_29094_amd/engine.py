@@ -124,6 +124,19 @@ class Request:
         return self.k * self.block >= self.gen_len
 
 
+def advance(r: Request, unmasked: int) -> None:
+    """Host bookkeeping after a step that unmasked `unmasked` positions of r's
+    active block: a block is done when none of its positions is masked, and
+    the next step of the request is then the recompute step of the next block."""
+    r.steps += 1
+    r.unmasked += unmasked
+    r.masked_in_block -= unmasked
+    if r.masked_in_block <= 0:
+        r.k += 1
+        if not r.done:
+            r.masked_in_block = r.block_len
+
+
 class Engine:
     """Slots, workspace and packed token/mask buffers for a fixed set of slots."""
 
@@ -234,13 +247,7 @@ class Engine:
             torch.cuda.ExternalStream(stream).synchronize()
         counts = self.host_n[:n].tolist()
         for r, c in zip(reqs, counts):
-            r.steps += 1
-            r.unmasked += c
-            r.masked_in_block -= c
-            if r.masked_in_block <= 0:
-                r.k += 1
-                if not r.done:
-                    r.masked_in_block = r.block_len
+            advance(r, c)
         return counts
 
     def step(self, reqs: List[Request], stream=None):
@@ -283,6 +290,18 @@ class Engine:
         if self.stats is not None:
             out["stats"] = self.stats[:n_req * dlm.DLM_NSTATS].view(n_req, dlm.DLM_NSTATS).cpu().numpy()
         return out
+
+    def save_state(self, req: Request):
+        """Host copy of what a request needs to resume elsewhere (tokens, mask,
+        token confidences, block index): a few bytes per position, no KV."""
+        toks, msk = self.read_state(req)
+        tc = None if self.tok_conf is None else self.read_tok_conf(req)
+        return (toks, msk.astype(np.uint8), tc, req.k)
+
+    def restore_state(self, req: Request, state) -> None:
+        """After admit(): put a saved request back; its next step is a recompute."""
+        toks, msk, tc, k = state
+        self.set_state(req, toks, msk, k, tc)
 
     def read_tok_conf(self, req: Request) -> np.ndarray:
         o = req.tok_offset
