@@ -171,14 +171,16 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 }
 
 // Tile/split choice. bf16 with K a multiple of 64 uses the direct-load kernel.
-// A configuration keeps `occ` blocks per CU resident; a full round of them
-// over K = 4096 takes t_round microseconds (fitted to launches whose weights
-// stream from HBM, MI355X). A last, partly filled round of a multi-block
-// configuration costs max(0.7, fill) of a full one (a lone 4-wave block on a
-// CU is latency-bound). Estimate = rounds x t_round x (K slice / 4096), plus
-// the HBM traffic of the fp32 K slices when K is split (written by the GEMM,
-// read back by the consumer); the cheapest (configuration, split) wins.
-// group_m selects the tile order (see gemm_dl_kernel).
+// A configuration keeps `occ` blocks per CU resident. Its time is modelled as
+// rounds x (a + b x k-tiles per block) microseconds, (a, b) fitted per
+// configuration to 768 launches on MI355X (the projection shapes of both model
+// shapes at M = 256 .. 8192, every split, weights streamed from HBM; launches
+// with M <= 1024 weighted double); a last,
+// partly filled round of a multi-block configuration costs max(0.7, fill) of a
+// full one. When K is split, the fp32 slices add their HBM traffic (written by
+// the GEMM, read back by the consumer). The cheapest (configuration, split)
+// wins. 128x192 (cfg 22) runs without K splits only; the small tiles only for
+// few rows.
 GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
   GemmPlan best{-1, 1, 0};
   if (M <= 0 || N <= 0) return best;
@@ -193,12 +195,13 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
     }
     return best;
   }
-  // 128x192 (cfg 22) is used only without K splits: measured slower than
-  // 128x128 on the N = 4096 projections it would otherwise win in the model.
-  struct Cand { int cfg; int occ; double t_round; int max_m; bool unsplit_only; };
-  const Cand cands[] = {{21, 1, 105.0, 1 << 30, false}, {22, 2, 100.0, 1 << 30, true},
-                        {6, 1, 124.0, 1 << 30, false}, {1, 2, 90.0, 1 << 30, false},
-                        {10, 3, 75.0, 64, false}};
+  struct Cand { int cfg; int occ; double a, b; int max_m; bool unsplit_only; };
+  const Cand cands[] = {{6, 1, -12.14, 1.919, 1 << 30, false},
+                        {21, 1, -5.93, 1.511, 1 << 30, false},
+                        {22, 2, -6.63, 1.681, 1 << 30, true},
+                        {29, 1, -4.72, 1.093, 1 << 30, false},
+                        {1, 2, -3.96, 1.271, 128, false},
+                        {10, 3, 0.0, 1.17, 64, false}};
   double best_t = 1e30;
   for (const Cand& c : cands) {
     if (M > c.max_m || (c.unsplit_only && splittable)) continue;
@@ -212,12 +215,26 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
       const double fill = (double)(units - full * slots) / slots;
       double rounds = (double)full;
       if (fill > 0) rounds += c.occ > 1 ? std::max(0.7, fill) : 1.0;
-      double t = rounds * c.t_round * (double)(K / s) / 4096.0;
+      double t = rounds * (c.a + c.b * (double)(K / s) / 64.0);
       if (s > 1) t += (double)M * N * 4.0 * 2.0 * (s - 1) / 5.0e12 * 1e6;
       if (t < best_t * 0.999) {
         best_t = t;
         best = GemmPlan{c.cfg, s, 0};
       }
+    }
+  }
+  // 128x192 with two blocks on every CU measured faster than the model says
+  // (by up to ~10 % at 512 - 2048 rows): take it within 12 % of the estimate
+  if (!splittable && best_t < 1e30) {
+    int bm22, bn22, th22;
+    gemm_dl_tile(22, &bm22, &bn22, &th22);
+    const long units = (long)ceil_div(M, bm22) * ceil_div(N, bn22);
+    const long slots = 2L * num_cu;
+    if (units >= slots) {
+      const long full = units / slots;
+      const double fill = (double)(units - full * slots) / slots;
+      const double rounds = full + (fill > 0 ? std::max(0.7, fill) : 0.0);
+      if (rounds * (-6.63 + 1.681 * (double)K / 64.0) <= best_t * 1.12) best = GemmPlan{22, 1, 0};
     }
   }
   // weights larger than the last-level cache (256 MB Infinity Cache) stream

@@ -189,7 +189,12 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   X(20, 64, 128, 2, 2, 4, 64)    \
   X(21, 256, 192, 4, 2, 2, 128)  \
   X(22, 128, 192, 2, 2, 2, 128)  \
-  X(23, 256, 192, 2, 2, 2, 128)
+  X(23, 256, 192, 2, 2, 2, 128)  \
+  X(27, 256, 256, 2, 4, 2, 64)   \
+  X(28, 128, 256, 2, 4, 3, 128)  \
+  X(29, 256, 128, 4, 2, 3, 128)  \
+  X(30, 128, 192, 2, 2, 3, 128)  \
+  X(31, 128, 192, 2, 2, 4, 128)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
