@@ -173,7 +173,7 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // Tile/split choice. bf16 with K a multiple of 64 uses the direct-load kernel.
 // A configuration keeps `occ` blocks per CU resident. Its time is modelled as
 // rounds x (a + b x k-tiles per block) microseconds, (a, b) fitted per
-// configuration to 768 launches on MI355X (the projection shapes of both model
+// configuration to 1096 launches on MI355X (the projection shapes of both model
 // shapes at M = 256 .. 8192, every split, weights streamed from HBM; launches
 // with M <= 1024 weighted double); a last,
 // partly filled round of a multi-block configuration costs max(0.7, fill) of a
@@ -196,11 +196,12 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
     return best;
   }
   struct Cand { int cfg; int occ; double a, b; int max_m; bool unsplit_only; };
-  const Cand cands[] = {{6, 1, -12.14, 1.919, 1 << 30, false},
-                        {21, 1, -5.93, 1.511, 1 << 30, false},
-                        {22, 2, -6.63, 1.681, 1 << 30, true},
-                        {29, 1, -4.72, 1.093, 1 << 30, false},
-                        {1, 2, -3.96, 1.271, 128, false},
+  const Cand cands[] = {{6, 1, -11.51, 1.867, 1 << 30, false},
+                        {21, 1, -6.35, 1.443, 1 << 30, false},
+                        {22, 2, 2.19, 1.458, 1 << 30, true},
+                        {29, 1, -4.43, 1.111, 1 << 30, false},
+                        {42, 1, 0.23, 0.918, 1 << 30, false},
+                        {1, 2, -4.15, 1.255, 128, false},
                         {10, 3, 0.0, 1.17, 64, false}};
   double best_t = 1e30;
   for (const Cand& c : cands) {
@@ -221,20 +222,6 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
         best_t = t;
         best = GemmPlan{c.cfg, s, 0};
       }
-    }
-  }
-  // 128x192 with two blocks on every CU measured faster than the model says
-  // (by up to ~10 % at 512 - 2048 rows): take it within 12 % of the estimate
-  if (!splittable && best_t < 1e30) {
-    int bm22, bn22, th22;
-    gemm_dl_tile(22, &bm22, &bn22, &th22);
-    const long units = (long)ceil_div(M, bm22) * ceil_div(N, bn22);
-    const long slots = 2L * num_cu;
-    if (units >= slots) {
-      const long full = units / slots;
-      const double fill = (double)(units - full * slots) / slots;
-      const double rounds = full + (fill > 0 ? std::max(0.7, fill) : 0.0);
-      if (rounds * (-6.63 + 1.681 * (double)K / 64.0) <= best_t * 1.12) best = GemmPlan{22, 1, 0};
     }
   }
   // weights larger than the last-level cache (256 MB Infinity Cache) stream

@@ -5,9 +5,11 @@
 // of that kilobyte, and it fetches the global 16-byte chunk that belongs
 // there under an XOR swizzle (LDS chunk slot = global chunk ^ (row & 7)), so
 // that the 16 lanes that later read 16 consecutive rows of one chunk hit
-// distinct banks. Loads go STAGES-1 k-tiles ahead through a ring of LDS stages;
-// no registers hold tiles in flight. The MFMA part and the epilogues are the
-// same as the register-staged kernel.
+// distinct banks. The weight operand B goes SB-1 k-tiles ahead through a ring of
+// SB LDS stages and the activation operand A one k-tile ahead through two (A
+// is re-read by every column tile and mostly served from cache; B streams from
+// HBM and needs the deeper prefetch); no registers hold tiles in flight. The
+// MFMA part and the epilogues are the same as the register-staged kernel.
 #include "common.h"
 #include "gemm_common.h"
 #include "kernels.h"
@@ -26,11 +28,13 @@ typedef __attribute__((address_space(3))) void* lptr_t;
 
 constexpr int kXcds = 8;      // XCDs the dispatcher spreads blocks over
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int RB, class Epi>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SB, int RB, class Epi>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int k_per_split, int group_m, Epi epi) {
   static_assert(RB == 64 || RB == 128, "k-tile row bytes");
+  static_assert(SB >= 2 && SB <= 4, "B stages");
+  constexpr int SA = 2;                   // A (activation) stages
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   constexpr int FM = TM / 16, FN = TN / 16;
@@ -38,13 +42,12 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   constexpr int CPR = RB / 16;            // 16-byte chunks per row
   constexpr int RPI = 1024 / RB;          // rows per 1 KB wave instruction
   constexpr int KG = RB / 64;             // 32-wide k groups per k-tile
-  constexpr int ROWS = BM + BN;
-  constexpr int STAGE = ROWS * RB;
-  constexpr int INSTR = ROWS / RPI;
-  static_assert(INSTR % NW == 0, "rows per wave");
-  constexpr int PERW = INSTR / NW;
-  static_assert(STAGES >= 2 && (STAGES - 2) * PERW < 64, "stages");
-  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+  constexpr int STAGE_A = BM * RB, STAGE_B = BN * RB;
+  constexpr int PERW_A = BM / RPI / NW, PERW_B = BN / RPI / NW;
+  static_assert(PERW_A * NW * RPI == BM && PERW_B * NW * RPI == BN, "rows per wave");
+  static_assert(PERW_B < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) char smem[SA * STAGE_A + SB * STAGE_B];
+  char* const smem_b = smem + SA * STAGE_A;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -86,24 +89,32 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   // (two per 128-byte bank line for 64-byte rows) map to distinct banks.
   auto swz = [](int r) { return CPR == 8 ? (r & 7) : ((r >> 1) & 3); };
   // source of this lane for each of its wave's instructions (fixed over k)
-  const bf16* src[PERW];
+  const bf16* srcA[PERW_A];
+  const bf16* srcB[PERW_B];
 #pragma unroll
-  for (int j = 0; j < PERW; ++j) {
-    const int row = RPI * (wave * PERW + j) + lane / CPR;
+  for (int j = 0; j < PERW_A; ++j) {
+    const int row = RPI * (wave * PERW_A + j) + lane / CPR;
     const int cc = (lane % CPR) ^ swz(row);
-    if (row < BM) {
-      const int m = min(m0 + row, M - 1);
-      src[j] = A + (long)m * lda + kbeg + cc * 8;
-    } else {
-      const int n = min(n0 + row - BM, N - 1);
-      src[j] = B + (long)epi.b_row(n) * ldb + kbeg + cc * 8;
-    }
+    srcA[j] = A + (long)min(m0 + row, M - 1) * lda + kbeg + cc * 8;
   }
-  auto issue = [&](int stage, int kt) {
-    char* dst = smem + stage * STAGE + wave * PERW * 1024;
 #pragma unroll
-    for (int j = 0; j < PERW; ++j)
-      __builtin_amdgcn_global_load_lds((gptr_t)(src[j] + kt * BK), (lptr_t)(dst + j * 1024), 16,
+  for (int j = 0; j < PERW_B; ++j) {
+    const int row = RPI * (wave * PERW_B + j) + lane / CPR;
+    const int cc = (lane % CPR) ^ swz(row);
+    srcB[j] = B + (long)epi.b_row(min(n0 + row, N - 1)) * ldb + kbeg + cc * 8;
+  }
+  auto issue_a = [&](int stage, int kt) {
+    char* dst = smem + stage * STAGE_A + wave * PERW_A * 1024;
+#pragma unroll
+    for (int j = 0; j < PERW_A; ++j)
+      __builtin_amdgcn_global_load_lds((gptr_t)(srcA[j] + kt * BK), (lptr_t)(dst + j * 1024), 16,
+                                       0, 0);
+  };
+  auto issue_b = [&](int stage, int kt) {
+    char* dst = smem_b + stage * STAGE_B + wave * PERW_B * 1024;
+#pragma unroll
+    for (int j = 0; j < PERW_B; ++j)
+      __builtin_amdgcn_global_load_lds((gptr_t)(srcB[j] + kt * BK), (lptr_t)(dst + j * 1024), 16,
                                        0, 0);
   };
 
@@ -116,22 +127,23 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   // fragment offsets: row R = base + (lane & 15) with base a multiple of 16,
   // chunk c = 4 g + lane / 16, stored at slot c ^ swz(R) = c ^ swz(lane & 15)
   const int a_row = (wm * TM + (lane & 15)) * RB;
-  const int b_row = (BM + wn * TN + (lane & 15)) * RB;
+  const int b_row = (wn * TN + (lane & 15)) * RB;
   int co[KG];
 #pragma unroll
   for (int g = 0; g < KG; ++g) co[g] = ((g * 4 + (lane >> 4)) ^ swz(lane & 15)) << 4;
 
-  auto compute = [&](int stage) {
-    const char* s = smem + stage * STAGE;
+  auto compute = [&](int sa, int sb) {
+    const char* pa = smem + sa * STAGE_A;
+    const char* pb = smem_b + sb * STAGE_B;
 #pragma unroll
     for (int g = 0; g < KG; ++g) {
       u32x4 af[FM], bfr[FN];
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
-        af[fm] = *reinterpret_cast<const u32x4*>(s + a_row + fm * 16 * RB + co[g]);
+        af[fm] = *reinterpret_cast<const u32x4*>(pa + a_row + fm * 16 * RB + co[g]);
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn)
-        bfr[fn] = *reinterpret_cast<const u32x4*>(s + b_row + fn * 16 * RB + co[g]);
+        bfr[fn] = *reinterpret_cast<const u32x4*>(pb + b_row + fn * 16 * RB + co[g]);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -141,60 +153,45 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     }
   };
 
+  // Pipeline: weights (B) run SB - 1 k-tiles ahead through an SB-stage ring,
+  // activations (A, mostly cache-resident) one k-tile ahead through two
+  // stages. Issue order: B(0) .. B(SB-2), A(0); then iteration kt issues
+  // A(kt+1) followed by B(kt+SB-1). At the top of iteration kt the loads that
+  // may still be in flight are exactly those issued after A(kt): B(kt+SB-2)
+  // when SB >= 3 (vmcnt counts this wave's loads in issue order).
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nkt) issue(s, s);
+  for (int t = 0; t < SB - 1; ++t)
+    if (t < nkt) issue_b(t, t);
+  if (nkt > 0) issue_a(0, 0);
 
   for (int kt = 0; kt < nkt; ++kt) {
-    // tiles kt+1 .. min(nkt-1, kt+STAGES-2) may stay in flight
-    const int ahead = min(STAGES - 2, nkt - 1 - kt);
-    if constexpr (STAGES == 2) {
-      wait_vmcnt<0>();
-    } else if constexpr (STAGES == 3) {
-      if (ahead >= 1) wait_vmcnt<PERW>(); else wait_vmcnt<0>();
-    } else if constexpr (STAGES == 4) {
-      if (ahead >= 2) wait_vmcnt<2 * PERW>();
-      else if (ahead == 1) wait_vmcnt<PERW>();
-      else wait_vmcnt<0>();
+    if constexpr (SB >= 3) {
+      if (kt > 0 && kt + SB - 2 < nkt) wait_vmcnt<PERW_B>(); else wait_vmcnt<0>();
     } else {
-      static_assert(STAGES == 5, "2..5 stages");
-      if (ahead >= 3) wait_vmcnt<3 * PERW>();
-      else if (ahead == 2) wait_vmcnt<2 * PERW>();
-      else if (ahead == 1) wait_vmcnt<PERW>();
-      else wait_vmcnt<0>();
+      wait_vmcnt<0>();
     }
     // Every wave has its own loads of tile kt in LDS and has finished reading
-    // the stage about to be refilled. A bare s_barrier: __syncthreads() would
-    // add a fence that drains every load in flight.
+    // the stages about to be refilled (read at kt - 1). A bare s_barrier:
+    // __syncthreads() would add a fence that drains every load in flight.
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if (kt + STAGES - 1 < nkt) issue((kt + STAGES - 1) % STAGES, kt + STAGES - 1);
-    compute(kt % STAGES);
+    if (kt + 1 < nkt) issue_a((kt + 1) & 1, kt + 1);
+    if (kt + SB - 1 < nkt) issue_b((kt + SB - 1) % SB, kt + SB - 1);
+    compute(kt & 1, kt % SB);
   }
   __syncthreads();
   epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
 }
 
-// Tile configurations (BM, BN, waves M x N, stages, k-tile row bytes).
+// Tile configurations (BM, BN, waves M x N, weight stages, k-tile row bytes).
 #define DL_CONFIGS(X)            \
   X(1, 128, 128, 2, 2, 2, 128)   \
   X(6, 256, 256, 2, 4, 2, 128)   \
   X(10, 64, 128, 2, 2, 2, 128)   \
-  X(14, 256, 256, 2, 4, 4, 64)   \
-  X(15, 256, 256, 2, 4, 3, 64)   \
-  X(16, 128, 128, 2, 2, 4, 64)   \
-  X(17, 128, 128, 2, 2, 3, 64)   \
-  X(18, 128, 256, 2, 4, 4, 64)   \
-  X(19, 256, 128, 4, 2, 4, 64)   \
-  X(20, 64, 128, 2, 2, 4, 64)    \
   X(21, 256, 192, 4, 2, 2, 128)  \
   X(22, 128, 192, 2, 2, 2, 128)  \
-  X(23, 256, 192, 2, 2, 2, 128)  \
-  X(27, 256, 256, 2, 4, 2, 64)   \
-  X(28, 128, 256, 2, 4, 3, 128)  \
   X(29, 256, 128, 4, 2, 3, 128)  \
-  X(30, 128, 192, 2, 2, 3, 128)  \
-  X(31, 128, 192, 2, 2, 4, 128)
+  X(42, 128, 192, 2, 2, 3, 128)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
