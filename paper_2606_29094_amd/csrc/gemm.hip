@@ -171,16 +171,57 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 }
 
 // Tile/split choice. bf16 with K a multiple of 64 uses the direct-load kernel.
-// A configuration keeps `occ` blocks per CU resident. Its time is modelled as
-// rounds x (a + b x k-tiles per block) microseconds, (a, b) fitted per
-// configuration to 1096 launches on MI355X (the projection shapes of both model
-// shapes at M = 256 .. 8192, every split, weights streamed from HBM; launches
-// with M <= 1024 weighted double); a last,
-// partly filled round of a multi-block configuration costs max(0.7, fill) of a
-// full one. When K is split, the fp32 slices add their HBM traffic (written by
-// the GEMM, read back by the consumer). The cheapest (configuration, split)
-// wins. 128x192 (cfg 22) runs without K splits only; the small tiles only for
-// few rows.
+// A configuration keeps `occ` blocks per CU resident. Its time is rounds x
+// (time of one round at the block's k-tile count), the per-round times being
+// medians of 1096 launches measured on MI355X (the projection shapes of both
+// model shapes at M = 256 .. 8192, every split, weights streamed from HBM),
+// interpolated linearly in k-tiles (proportionally outside the measured range);
+// a last, partly filled round of a multi-block configuration costs
+// max(0.7, fill) of a full one. When K is split, the fp32 slices add their HBM
+// traffic (written by the GEMM, read back by the consumer). The cheapest
+// (configuration, split) wins. 128x192 with two blocks per CU (cfg 22) runs
+// without K splits only; the small tiles only for few rows.
+namespace {
+struct RoundTable {
+  int cfg, occ, max_m;
+  bool unsplit_only;
+  int n;
+  float kt[15], us[15];
+};
+const RoundTable kRoundTables[] = {
+    {6, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {25.6f, 32.2f, 38.6f, 55.3f, 51.4f, 63.7f, 77.7f, 93.6f, 97.4f, 115.0f, 134.6f, 165.2f, 246.0f, 301.5f, 457.3f}},
+    {21, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {20.0f, 26.2f, 29.9f, 42.5f, 42.0f, 48.4f, 60.3f, 71.5f, 76.1f, 91.4f, 103.4f, 128.4f, 194.9f, 246.0f, 377.2f}},
+    {22, 2, 1 << 30, true, 4, {56, 64, 192, 296}, {83.1f, 95.4f, 281.2f, 433.6f}},
+    {29, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {16.3f, 19.6f, 23.3f, 32.5f, 32.3f, 38.6f, 47.5f, 55.5f, 60.4f, 72.0f, 82.6f, 103.4f, 149.0f, 195.0f, 287.4f}},
+    {42, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {15.1f, 19.1f, 21.2f, 30.1f, 29.8f, 33.6f, 42.0f, 50.2f, 52.0f, 59.5f, 74.2f, 86.3f, 133.4f, 161.7f, 251.7f}},
+    {43, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {16.3f, 19.8f, 23.0f, 32.2f, 31.9f, 37.9f, 47.2f, 55.6f, 57.5f, 68.5f, 84.1f, 102.1f, 148.1f, 188.5f, 284.5f}},
+    {1, 2, 128, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {17.2f, 24.1f, 25.3f, 37.7f, 35.3f, 42.2f, 52.8f, 66.0f, 66.4f, 73.3f, 92.4f, 118.7f, 172.0f, 215.7f, 336.2f}},
+    {10, 3, 64, false, 1, {64}, {75.0f}},
+};
+
+double round_us(const RoundTable& t, double kt) {
+  if (kt <= t.kt[0]) return t.us[0] * kt / t.kt[0];
+  for (int i = 1; i < t.n; ++i)
+    if (kt <= t.kt[i]) {
+      const double w = (kt - t.kt[i - 1]) / (t.kt[i] - t.kt[i - 1]);
+      return t.us[i - 1] + w * (t.us[i] - t.us[i - 1]);
+    }
+  return t.us[t.n - 1] * kt / t.kt[t.n - 1];
+}
+}  // namespace
+
 GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
   GemmPlan best{-1, 1, 0};
   if (M <= 0 || N <= 0) return best;
@@ -195,16 +236,8 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
     }
     return best;
   }
-  struct Cand { int cfg; int occ; double a, b; int max_m; bool unsplit_only; };
-  const Cand cands[] = {{6, 1, -11.51, 1.867, 1 << 30, false},
-                        {21, 1, -6.35, 1.443, 1 << 30, false},
-                        {22, 2, 2.19, 1.458, 1 << 30, true},
-                        {29, 1, -4.43, 1.111, 1 << 30, false},
-                        {42, 1, 0.23, 0.918, 1 << 30, false},
-                        {1, 2, -4.15, 1.255, 128, false},
-                        {10, 3, 0.0, 1.17, 64, false}};
   double best_t = 1e30;
-  for (const Cand& c : cands) {
+  for (const RoundTable& c : kRoundTables) {
     if (M > c.max_m || (c.unsplit_only && splittable)) continue;
     int bm, bn, th;
     gemm_dl_tile(c.cfg, &bm, &bn, &th);
@@ -216,7 +249,7 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
       const double fill = (double)(units - full * slots) / slots;
       double rounds = (double)full;
       if (fill > 0) rounds += c.occ > 1 ? std::max(0.7, fill) : 1.0;
-      double t = rounds * (c.a + c.b * (double)(K / s) / 64.0);
+      double t = rounds * round_us(c, (double)(K / s) / 64.0);
       if (s > 1) t += (double)M * N * 4.0 * 2.0 * (s - 1) / 5.0e12 * 1e6;
       if (t < best_t * 0.999) {
         best_t = t;

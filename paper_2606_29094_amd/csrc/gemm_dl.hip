@@ -191,7 +191,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   X(21, 256, 192, 4, 2, 2, 128)  \
   X(22, 128, 192, 2, 2, 2, 128)  \
   X(29, 256, 128, 4, 2, 3, 128)  \
-  X(42, 128, 192, 2, 2, 3, 128)
+  X(42, 128, 192, 2, 2, 3, 128)  \
+  X(43, 256, 128, 4, 2, 4, 128)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
