@@ -53,6 +53,16 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
 // h[n] += sum_s part[s][n] (slices in order), so the residual update of the
 // previous projection and this norm take one pass over h. out may be null
 // (update only). rows/count select and bound the rows (final-norm gather).
+// four consecutive outputs in one 16-byte (fp32) or 8-byte (bf16) store
+__device__ __forceinline__ void store4(float* o, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(o) = make_float4(a, b, c, d);
+}
+__device__ __forceinline__ void store4(bf16* o, float a, float b, float c, float d) {
+  bf16x4 v;
+  v[0] = (bf16)a; v[1] = (bf16)b; v[2] = (bf16)c; v[3] = (bf16)d;
+  *reinterpret_cast<bf16x4*>(o) = v;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ h,
                                                       const float* __restrict__ part, int splits,
@@ -66,6 +76,58 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ h,
   const int src_row = rows ? rows[i] : i;
   float* x = h + (long)src_row * d;
   float ss = 0.f;
+  if (d <= 4096) {
+    // rows of up to 4096: the thread's (at most) four float4 stay in registers
+    // between the update and the normalisation; all loads of a slice are issued
+    // together
+    float4 v[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int j = threadIdx.x * 4 + c * 1024;
+      if (j < d) v[c] = *reinterpret_cast<const float4*>(x + j);
+    }
+    if (part) {
+      for (int sl = 0; sl < splits; ++sl) {
+        const float* ps = part + sl * stride + (long)src_row * d;
+        float4 pv[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int j = threadIdx.x * 4 + c * 1024;
+          if (j < d) pv[c] = *reinterpret_cast<const float4*>(ps + j);
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int j = threadIdx.x * 4 + c * 1024;
+          if (j < d) {
+            v[c].x += pv[c].x; v[c].y += pv[c].y; v[c].z += pv[c].z; v[c].w += pv[c].w;
+          }
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int j = threadIdx.x * 4 + c * 1024;
+        if (j < d) *reinterpret_cast<float4*>(x + j) = v[c];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int j = threadIdx.x * 4 + c * 1024;
+      if (j < d) ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
+    }
+    if (!out) return;
+    const float inv = 1.0f / sqrtf(block_sum_256(ss, red) / (float)d + eps);
+    T* o = out + (long)i * d;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int j = threadIdx.x * 4 + c * 1024;
+      if (j < d) {
+        const float4 gg = *reinterpret_cast<const float4*>(g + j);
+        store4(o + j, v[c].x * inv * gg.x, v[c].y * inv * gg.y, v[c].z * inv * gg.z,
+               v[c].w * inv * gg.w);
+      }
+    }
+    return;
+  }
   for (int j = threadIdx.x * 4; j < d; j += 1024) {
     float4 v = *reinterpret_cast<const float4*>(x + j);
     if (part) {
