@@ -243,14 +243,10 @@ __global__ __launch_bounds__(256) void qkv_rope_scatter_kernel(
       const float4 c01 = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i);
       const float4 c23 = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i + 2);
       T* o = dst_base + (kv ? (long)(pos_base + rr) : (long)n) * dst_row_stride;
-      o[i + 0] = from_f32<T>(a.x * c01.x - b.x * c01.y);
-      o[i + 1] = from_f32<T>(a.y * c01.z - b.y * c01.w);
-      o[i + 2] = from_f32<T>(a.z * c23.x - b.z * c23.y);
-      o[i + 3] = from_f32<T>(a.w * c23.z - b.w * c23.w);
-      o[i + HALF + 0] = from_f32<T>(b.x * c01.x + a.x * c01.y);
-      o[i + HALF + 1] = from_f32<T>(b.y * c01.z + a.y * c01.w);
-      o[i + HALF + 2] = from_f32<T>(b.z * c23.x + a.z * c23.y);
-      o[i + HALF + 3] = from_f32<T>(b.w * c23.z + a.w * c23.w);
+      store4(o + i, a.x * c01.x - b.x * c01.y, a.y * c01.z - b.y * c01.w,
+             a.z * c23.x - b.z * c23.y, a.w * c23.z - b.w * c23.w);
+      store4(o + i + HALF, b.x * c01.x + a.x * c01.y, b.y * c01.z + a.y * c01.w,
+             b.z * c23.x + a.z * c23.y, b.w * c23.z + a.w * c23.w);
     }
   };
   if (y < hq) {
