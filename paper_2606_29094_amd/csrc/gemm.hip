@@ -173,7 +173,7 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // Tile/split choice. bf16 with K a multiple of 64 uses the direct-load kernel.
 // A configuration keeps `occ` blocks per CU resident. Its time is rounds x
 // (time of one round at the block's k-tile count), the per-round times being
-// medians of 1096 launches measured on MI355X (the projection shapes of both
+// medians of 757 launches measured on MI355X (the projection shapes of both
 // model shapes at M = 256 .. 8192, every split, weights streamed from HBM),
 // interpolated linearly in k-tiles (proportionally outside the measured range);
 // a last, partly filled round of a multi-block configuration costs
@@ -191,23 +191,23 @@ struct RoundTable {
 const RoundTable kRoundTables[] = {
     {6, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {25.6f, 32.2f, 38.6f, 55.3f, 51.4f, 63.7f, 77.7f, 93.6f, 97.4f, 115.0f, 134.6f, 165.2f, 246.0f, 301.5f, 457.3f}},
+     {24.8f, 30.1f, 36.3f, 51.8f, 48.5f, 58.8f, 75.5f, 85.9f, 89.7f, 106.1f, 130.4f, 151.4f, 227.9f, 279.8f, 430.1f}},
     {21, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {20.0f, 26.2f, 29.9f, 42.5f, 42.0f, 48.4f, 60.3f, 71.5f, 76.1f, 91.4f, 103.4f, 128.4f, 194.9f, 246.0f, 377.2f}},
-    {22, 2, 1 << 30, true, 4, {56, 64, 192, 296}, {83.1f, 95.4f, 281.2f, 433.6f}},
+     {19.6f, 25.4f, 28.3f, 41.6f, 40.8f, 46.9f, 60.5f, 69.6f, 72.6f, 86.6f, 102.3f, 127.4f, 188.4f, 240.1f, 368.8f}},
+    {22, 2, 1 << 30, true, 4, {56, 64, 192, 296}, {81.9f, 93.1f, 282.1f, 435.5f}},
     {29, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {16.3f, 19.6f, 23.3f, 32.5f, 32.3f, 38.6f, 47.5f, 55.5f, 60.4f, 72.0f, 82.6f, 103.4f, 149.0f, 195.0f, 287.4f}},
+     {15.9f, 18.6f, 22.8f, 31.9f, 31.3f, 37.1f, 46.3f, 54.8f, 58.0f, 71.1f, 81.9f, 99.7f, 147.8f, 193.6f, 284.2f}},
     {42, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {15.1f, 19.1f, 21.2f, 30.1f, 29.8f, 33.6f, 42.0f, 50.2f, 52.0f, 59.5f, 74.2f, 86.3f, 133.4f, 161.7f, 251.7f}},
+     {14.6f, 18.1f, 20.7f, 29.2f, 27.6f, 32.4f, 41.1f, 47.7f, 47.8f, 56.8f, 70.6f, 80.0f, 124.7f, 154.4f, 232.9f}},
     {43, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {16.3f, 19.8f, 23.0f, 32.2f, 31.9f, 37.9f, 47.2f, 55.6f, 57.5f, 68.5f, 84.1f, 102.1f, 148.1f, 188.5f, 284.5f}},
+     {15.8f, 18.7f, 22.3f, 31.5f, 29.9f, 36.6f, 47.5f, 53.7f, 55.9f, 66.4f, 81.5f, 97.3f, 145.2f, 183.3f, 279.2f}},
     {1, 2, 128, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {17.2f, 24.1f, 25.3f, 37.7f, 35.3f, 42.2f, 52.8f, 66.0f, 66.4f, 73.3f, 92.4f, 118.7f, 172.0f, 215.7f, 336.2f}},
+     {17.1f, 22.4f, 25.6f, 37.3f, 33.5f, 40.8f, 51.1f, 65.7f, 65.8f, 71.1f, 90.8f, 119.1f, 171.0f, 214.9f, 335.1f}},
     {10, 3, 64, false, 1, {64}, {75.0f}},
 };
 

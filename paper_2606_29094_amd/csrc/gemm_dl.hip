@@ -135,21 +135,63 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   auto compute = [&](int sa, int sb) {
     const char* pa = smem + sa * STAGE_A;
     const char* pb = smem_b + sb * STAGE_B;
-#pragma unroll
-    for (int g = 0; g < KG; ++g) {
-      u32x4 af[FM], bfr[FN];
+    if constexpr (KG == 2) {
+      // Both k groups' fragments, then the MFMAs of group 0 with the reads of
+      // group 1 spread among them, then the MFMAs of group 1: the LDS latency
+      // of group 1 hides behind group 0's MFMAs (left to itself the compiler
+      // issues each read right before its first use and waits on it).
+      u32x4 af0[FM], bf0[FN], af1[FM], bf1[FN];
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
-        af[fm] = *reinterpret_cast<const u32x4*>(pa + a_row + fm * 16 * RB + co[g]);
+        af0[fm] = *reinterpret_cast<const u32x4*>(pa + a_row + fm * 16 * RB + co[0]);
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn)
-        bfr[fn] = *reinterpret_cast<const u32x4*>(pb + b_row + fn * 16 * RB + co[g]);
+        bf0[fn] = *reinterpret_cast<const u32x4*>(pb + b_row + fn * 16 * RB + co[0]);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+        af1[fm] = *reinterpret_cast<const u32x4*>(pa + a_row + fm * 16 * RB + co[1]);
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        bf1[fn] = *reinterpret_cast<const u32x4*>(pb + b_row + fn * 16 * RB + co[1]);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn)
-          acc[fm][fn] = mfma16_bf16(__builtin_bit_cast(bf16x8, af[fm]),
-                                    __builtin_bit_cast(bf16x8, bfr[fn]), acc[fm][fn]);
+          acc[fm][fn] = mfma16_bf16(__builtin_bit_cast(bf16x8, af0[fm]),
+                                    __builtin_bit_cast(bf16x8, bf0[fn]), acc[fm][fn]);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+          acc[fm][fn] = mfma16_bf16(__builtin_bit_cast(bf16x8, af1[fm]),
+                                    __builtin_bit_cast(bf16x8, bf1[fn]), acc[fm][fn]);
+      // scheduling groups (mask 0x100: LDS reads, 0x008: MFMA)
+      constexpr int NR = FM + FN, NM = FM * FN;
+      __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+#pragma unroll
+      for (int i = 0; i < NR; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NM / NR, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, NM - (NM / NR) * NR, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    } else {
+#pragma unroll
+      for (int g = 0; g < KG; ++g) {
+        u32x4 af[FM], bfr[FN];
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          af[fm] = *reinterpret_cast<const u32x4*>(pa + a_row + fm * 16 * RB + co[g]);
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+          bfr[fn] = *reinterpret_cast<const u32x4*>(pb + b_row + fn * 16 * RB + co[g]);
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn)
+            acc[fm][fn] = mfma16_bf16(__builtin_bit_cast(bf16x8, af[fm]),
+                                      __builtin_bit_cast(bf16x8, bfr[fn]), acc[fm][fn]);
+      }
     }
   };
 
