@@ -300,6 +300,250 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
   }
 }
 
+// Grouped-query attention (GH > 1 query heads per key/value head): one block
+// = the GH query heads of one key/value head x QG groups of 16 query rows of
+// one request, one wave per (query head, row group), so every staged K/V
+// tile serves GH * QG * 16 query rows. Tiles of 64 keys are fetched with
+// direct global->LDS loads into a two-stage ring: the next tile's loads run
+// during the current tile's MFMAs and no registers hold tiles in flight,
+// which keeps the register count low enough for two blocks per CU.
+//
+// LDS layout of a stage:
+//   K: 64 rows of DH. Row rho holds key pi(rho) of the tile, where inside each
+//      group of 32 keys pi(16 h + 4 g + i) = 8 g + 4 h + i (h < 2, g < 4,
+//      i < 4). With this order the S^T values a lane of lane group g owns
+//      are the keys 8 g .. 8 g + 7 of each 32-key group, which is the k slice
+//      that lane group supplies to the PV MFMA, so V^T is read as one
+//      16-byte chunk per lane and no shuffle is needed.
+//   V^T: DH rows of 64 keys (128 bytes).
+//   The 16-byte chunk c of row r is stored at chunk slot c ^ (r & 7): the
+//   eight lanes of one LDS read phase (one chunk of eight consecutive rows)
+//   hit distinct banks. Each lane of a load instruction fetches the global
+//   chunk that belongs at its slot.
+// Keys at or beyond L inside the last tile are read from the slot (a slot
+// holds s_max positions, a multiple of 64) and then masked: their scores are
+// set to -inf and their V^T entries cleared in LDS.
+template <int DH, int GH, int QG, bool PLO>
+__global__ __launch_bounds__(GH* QG * 64) void attn_gqa_kernel(StepPlan p, const bf16* __restrict__ q,
+                                                             const bf16* __restrict__ kc,
+                                                             const bf16* __restrict__ vc,
+                                                             int s_max, int hq, int hkv, int n_tiles,
+                                                             bf16* __restrict__ out,
+                                                             float scale_log2) {
+  constexpr int NW = GH * QG;              // waves
+  constexpr int NT = NW * 64;
+  constexpr int QT = 16 * QG;              // query rows per block
+  constexpr int SK = 64;                   // keys per tile
+  constexpr int KRB = DH * 2;              // K row bytes
+  constexpr int KCPR = DH / 8;             // 16-byte chunks per K row
+  constexpr int KRPI = 1024 / KRB;         // K rows per load instruction
+  constexpr int NKI = SK / KRPI;           // K load instructions per tile
+  constexpr int NVI = DH / 8;              // V^T load instructions per tile (8 rows each)
+  constexpr int NI = NKI + NVI;
+  constexpr int IPW = (NI + NW - 1) / NW;  // load instructions per wave (at most)
+  constexpr int KBYTES = SK * KRB;
+  constexpr int STAGE = KBYTES + DH * SK * 2;
+  constexpr int NDB = DH / 16;             // output dh blocks
+  constexpr int NKS = DH / 32;             // k steps of S
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+
+  // Block order: blocks are handed out in linear order round-robin over the
+  // XCDs; the linear id is remapped so that each XCD receives one contiguous
+  // range of (key/value head, query tile) with query tiles fastest, so the
+  // row tiles of one request and key/value head run on one XCD at about the
+  // same time and share its L2.
+  int kvh, tile;
+  {
+    const int total = gridDim.x, id = blockIdx.x;
+    const int xcd = id % kXcds, per = total / kXcds, rem = total % kXcds;
+    const int lid = xcd * per + min(xcd, rem) + id / kXcds;
+    kvh = lid / n_tiles;
+    tile = lid - kvh * n_tiles;
+  }
+  // request of this tile: tiles of QT rows are numbered request by request
+  int r = 0, t0 = 0;
+  for (; r + 1 < p.n_req; ++r) {
+    const int nt = (p.r[r].nrows + QT - 1) / QT;
+    if (tile < t0 + nt) break;
+    t0 += nt;
+  }
+  const ReqPlan& rq = p.r[r];
+  const int lrow0 = (tile - t0) * QT;
+  const int nvalid = min(QT, rq.nrows - lrow0);
+  const int L = rq.seq_len;
+  const bf16* kb = kc + ((long)(rq.slot * hkv + kvh) * s_max) * DH;
+  const bf16* vb = vc + ((long)(rq.slot * hkv + kvh) * DH) * s_max;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qg = wave % QG;                       // 16-row group
+  const int h = kvh * GH + wave / QG;             // query head
+  const int qr = qg * 16 + (lane & 15);           // query row of this lane in the tile
+  const bool q_ok = qr < nvalid;
+  const long qrow = rq.row0 + lrow0 + qr;
+  const int g = lane >> 4;
+
+  // this wave's load instructions: j = wave + NW m over the tile's NI
+  // instructions (the first NKI fill K, the rest V^T); per instruction the
+  // lane's source at key 0 of the slot and the LDS byte offset in the stage
+  const bf16* src[IPW];
+  int dst[IPW];
+#pragma unroll
+  for (int m = 0; m < IPW; ++m) {
+    const int j = wave + NW * m;
+    if (j < NKI) {
+      const int rho = KRPI * j + lane / KCPR;
+      const int c = (lane % KCPR) ^ (rho & 7);
+      const int key = (rho & ~31) | (((rho >> 2) & 3) << 3) | (((rho >> 4) & 1) << 2) | (rho & 3);
+      src[m] = kb + (long)key * DH + c * 8;
+      dst[m] = j * 1024;
+    } else {
+      const int jv = min(j, NI - 1) - NKI;
+      const int d = 8 * jv + lane / 8;
+      const int c = (lane % 8) ^ (d & 7);
+      src[m] = vb + (long)d * s_max + c * 8;
+      dst[m] = KBYTES + jv * 1024;
+    }
+  }
+  auto issue = [&](int stage, int key0) {
+    char* base = smem + stage * STAGE;
+#pragma unroll
+    for (int m = 0; m < IPW; ++m) {
+      const int j = wave + NW * m;
+      if (j < NI)
+        load_lds16(src[m] + (j < NKI ? (long)key0 * DH : (long)key0), base + dst[m]);
+    }
+  };
+
+  // Q fragments (B operand): col = query lane&15, k = dh 32*s + 8*g .. +7
+  u32x4 qf[NKS];
+#pragma unroll
+  for (int s = 0; s < NKS; ++s) {
+    if (q_ok)
+      qf[s] = *reinterpret_cast<const u32x4*>(q + qrow * hq * DH + h * DH + s * 32 + g * 8);
+    else
+      qf[s] = u32x4{0u, 0u, 0u, 0u};
+  }
+
+  f32x4 o[NDB];
+#pragma unroll
+  for (int i = 0; i < NDB; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_ref = -INFINITY, l_run = 0.f;
+  const int sw = (lane & 7) << 4;                 // chunk-slot XOR of rows 16 b + (lane & 15)
+
+  const int ntiles = ceil_div(L, SK);
+  issue(0, 0);
+  for (int t = 0; t < ntiles; ++t) {
+    const int key0 = t * SK;
+    wait_vmcnt<0>();
+    __syncthreads();                              // tile t in LDS; stage (t + 1) & 1 free
+    const char* kst = smem + (t & 1) * STAGE;
+    const char* vst = kst + KBYTES;
+    const bool tail = key0 + SK > L;
+    if (tail) {                                   // clear V^T at keys >= L
+      const int kl = L - key0;
+      for (int idx = tid; idx < DH * 8; idx += NT) {
+        const int d = idx >> 3, c = idx & 7;
+        if (8 * c + 8 > kl) {
+          u32x4* ptr = reinterpret_cast<u32x4*>(const_cast<char*>(vst) + d * 128 + ((c ^ (d & 7)) << 4));
+          u32x4 v = *ptr;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t keep = (8 * c + 2 * w < kl ? 0x0000ffffu : 0u) |
+                                  (8 * c + 2 * w + 1 < kl ? 0xffff0000u : 0u);
+            v[w] &= keep;
+          }
+          *ptr = v;
+        }
+      }
+      __syncthreads();
+    }
+    if (t + 1 < ntiles) issue((t + 1) & 1, key0 + SK);
+
+    // S^T blocks: sblk[kb][i] = raw score(key = key0 + pi(16 kb + 4 g + i), query = lane & 15)
+    f32x4 sblk[4];
+#pragma unroll
+    for (int kbk = 0; kbk < 4; ++kbk) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      const char* krow = kst + (kbk * 16 + (lane & 15)) * KRB;
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(krow + (((s * 4 + g) << 4) ^ sw));
+        acc = mfma16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, qf[s]), acc);
+      }
+      sblk[kbk] = acc;
+    }
+    if (tail) {
+#pragma unroll
+      for (int kbk = 0; kbk < 4; ++kbk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (key0 + 32 * (kbk >> 1) + 8 * g + 4 * (kbk & 1) + i >= L) sblk[kbk][i] = -INFINITY;
+    }
+    float mt = -INFINITY;
+#pragma unroll
+    for (int kbk = 0; kbk < 4; ++kbk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sblk[kbk][i]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    // move the reference maximum only on a large increase
+    const bool grow = (mt - m_ref) * scale_log2 > 8.0f;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float alpha = grow ? __builtin_amdgcn_exp2f((m_ref - mt) * scale_log2) : 1.0f;
+      if (grow) m_ref = mt;
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < NDB; ++i) o[i] *= alpha;
+    }
+    const float nm = m_ref == -INFINITY ? 0.0f : -m_ref * scale_log2;
+    float lsum = 0.f;
+#pragma unroll
+    for (int kbk = 0; kbk < 4; ++kbk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(sblk[kbk][i], scale_log2, nm));
+        sblk[kbk][i] = e;
+        lsum += e;
+      }
+    l_run += lsum;
+
+    // O^T += V^T P^T over two 32-key steps; B operand slot 8 g + e <-> key
+    // 32 j + 8 g + e, which lane group g holds as sblk[2 j + e / 4][e % 4]
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      bf16x8 ph, pl;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float pv = e < 4 ? sblk[2 * j][e] : sblk[2 * j + 1][e - 4];
+        ph[e] = (bf16)pv;
+        if constexpr (PLO) pl[e] = (bf16)(pv - (float)ph[e]);
+      }
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(vst + (db * 16 + (lane & 15)) * 128 +
+                                                        (((4 * j + g) << 4) ^ sw));
+        o[db] = mfma16_bf16(__builtin_bit_cast(bf16x8, a), ph, o[db]);
+        if constexpr (PLO) o[db] = mfma16_bf16(__builtin_bit_cast(bf16x8, a), pl, o[db]);
+      }
+    }
+  }
+
+  // finish: l over the 4 lanes sharing the query, normalise, store
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_run;
+  if (q_ok) {
+    bf16* dstp = out + qrow * hq * DH + h * DH;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (bf16)(o[db][i] * inv);
+      *reinterpret_cast<bf16x4*>(dstp + db * 16 + 4 * g) = v;
+    }
+  }
+}
+
 // fp32: one lane per query row; K and V^T tiles staged in LDS.
 template <int DH>
 __global__ __launch_bounds__(64) void attn_f32_kernel(StepPlan p, const float* __restrict__ q,
@@ -375,22 +619,49 @@ static hipError_t launch_attn(const StepPlan& p, const bf16* q, const bf16* kc, 
   return hipGetLastError();
 }
 
-// Query tiles of 32 rows when no request recomputes more than 32 rows (cache
-// steps of blocks <= 32), else 64; two key groups either way.
+template <int DH, int GH, int QG, bool PLO>
+static hipError_t launch_gqa(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
+                             int s_max, int hq, int hkv, bf16* out, float scale_log2,
+                             hipStream_t st) {
+  constexpr int QT = 16 * QG;
+  int tiles = 0;
+  for (int r = 0; r < p.n_req; ++r) tiles += (p.r[r].nrows + QT - 1) / QT;
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_gqa_kernel<DH, GH, QG, PLO>), dim3(hkv * tiles), dim3(GH * QG * 64), 0,
+                     st, p, q, kc, vc, s_max, hq, hkv, tiles, out, scale_log2);
+  return hipGetLastError();
+}
+
+// Grouped-query attention with 2, 4, 7 or 8 query heads per key/value head:
+// the shared-tile kernel with 7 or 8 waves per block; other head ratios and
+// MHA use the per-head kernel.
+template <int DH>
+static hipError_t attention_dh(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
+                               int s_max, int hq, int hkv, bf16* out, float scale_log2,
+                               hipStream_t st) {
+  switch (hkv > 0 && hq % hkv == 0 ? hq / hkv : 0) {
+    case 2: return launch_gqa<DH, 2, 4, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    case 4: return launch_gqa<DH, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    case 7: return launch_gqa<DH, 7, 1, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    case 8: return launch_gqa<DH, 8, 1, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    default: break;
+  }
+  // Query tiles of 32 rows when no request recomputes more than 32 rows
+  // (cache steps of blocks <= 32), else 64; two key groups either way.
+  int max_rows = 0;
+  for (int r = 0; r < p.n_req; ++r) max_rows = max(max_rows, p.r[r].nrows);
+  return max_rows <= 32
+             ? launch_attn<DH, 2, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
+             : launch_attn<DH, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+}
+
 template <>
 hipError_t attention<bf16>(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
                            int s_max, int hq, int hkv, int dh, bf16* out, hipStream_t st) {
   if (p.n_rows == 0) return hipSuccess;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
-  int max_rows = 0;
-  for (int r = 0; r < p.n_req; ++r) max_rows = max(max_rows, p.r[r].nrows);
-  const bool small = max_rows <= 32;
-  if (dh == 128)
-    return small ? launch_attn<128, 2, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
-                 : launch_attn<128, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
-  if (dh == 64)
-    return small ? launch_attn<64, 2, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
-                 : launch_attn<64, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+  if (dh == 128) return attention_dh<128>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+  if (dh == 64) return attention_dh<64>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
   return hipErrorInvalidValue;
 }
 

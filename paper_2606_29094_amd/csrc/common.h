@@ -50,4 +50,27 @@ __device__ __forceinline__ f32x4 mfma16_f32(float a, float b, const f32x4& c) {
 
 __host__ __device__ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// XCDs the dispatcher spreads a launch's blocks over (block i to XCD i mod 8);
+// each has its own L2
+constexpr int kXcds = 8;
+
+// ---- direct global -> LDS loads (global_load_lds_dwordx4) ----
+// One wave instruction moves 1 KB: lane l reads 16 bytes at its own global
+// address and writes them to LDS bytes [16 l, 16 l + 16) after the wave's
+// destination base. Completion is counted by vmcnt like any global load.
+typedef __attribute__((address_space(1))) const void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+
+__device__ __forceinline__ void load_lds16(const void* src, void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)lds_wave_base, 16, 0, 0);
+}
+
+// wait until at most N vector-memory operations of this wave are in flight
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt in [3:0] and [15:14]; expcnt (7) and lgkmcnt (15) not waited on
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 }  // namespace dlm

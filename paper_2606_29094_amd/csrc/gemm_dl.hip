@@ -16,18 +16,6 @@
 
 namespace dlm {
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  // gfx9 s_waitcnt: vmcnt in [3:0] and [15:14]; expcnt (7) and lgkmcnt (15) not waited on
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-typedef __attribute__((address_space(1))) const void* gptr_t;
-typedef __attribute__((address_space(3))) void* lptr_t;
-
-constexpr int kXcds = 8;      // XCDs the dispatcher spreads blocks over
-
 template <int BM, int BN, int WAVES_M, int WAVES_N, int SB, int RB, class Epi>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,

@@ -2,6 +2,8 @@
 and the comparison rules (tolerances and exemptions)."""
 from __future__ import annotations
 
+import copy
+
 import numpy as np
 import torch
 
@@ -135,3 +137,39 @@ def logit_err(z_gpu, z_ref):
 def top2_gap(z):
     s = np.sort(np.asarray(z, np.float64), axis=1)
     return s[:, -1] - s[:, -2]
+
+
+def calibrated_inv_tau(cfg, W, oreqs, mode):
+    """Calibrate on the oracle's first step of these requests (share 0.3 > 0.9)."""
+    zs = []
+    for oq in oreqs:
+        q = copy.deepcopy(oq)
+        h, rows, _ = oracle.step_forward(cfg, W, q, mode)
+        s, e = q.block_bounds
+        A = np.nonzero(q.mask[s:e])[0] + s
+        zs.append(oracle.head_logits(cfg, W, h[A - rows[0]], 1.0))
+    return float(oracle.calibrate(np.concatenate(zs), 0.9, 0.3)[1])
+
+
+def run_teacher_forced(cfg, W, eng, reqs, oreqs, mode, inv_tau, n_steps):
+    """n_steps batched steps; before each, every request is set to the
+    oracle's state; each request's step is compared with the oracle's."""
+    stats = {"lerr": 0.0, "cerr": 0.0, "exempt": 0, "kinds": []}
+    for _ in range(n_steps):
+        active = [i for i, oq in enumerate(oreqs) if not oq.done]
+        if not active:
+            break
+        for i in active:
+            eng.set_state(reqs[i], oreqs[i].tokens, oreqs[i].mask, oreqs[i].k)
+        flags = [reqs[i].refreshed_block != reqs[i].block_start for i in active]
+        z_rows, out, starts = gpu_step_with_logits(eng, [reqs[i] for i in active])
+        for j, i in enumerate(active):
+            res = oracle.denoise_step(cfg, W, oreqs[i], mode, inv_tau, keep_logits=True)
+            assert res.refresh == (flags[j] or mode == "none")
+            stats["kinds"].append(res.refresh)
+            l, c, e = check_step_e2e(res, {k: v[j] for k, v in out.items()}, starts[j],
+                                     reqs[i].threshold, z_rows[j])
+            stats["lerr"] = max(stats["lerr"], l)
+            stats["cerr"] = max(stats["cerr"], c)
+            stats["exempt"] += e
+    return stats

@@ -4,7 +4,6 @@ oracle with bf16 storage rounding: step logits (2e-2), confidences (bounded by
 each row's logit error, see helpers), unmask decisions, for no-cache,
 dual-cache and prefix-cache steps, ragged request lengths, short last blocks
 and batches that mix recompute and cache steps."""
-import copy
 import dataclasses
 
 import numpy as np
@@ -13,7 +12,7 @@ import pytest
 import oracle
 import synth
 import synth.device as sdev
-from helpers import check_step_e2e, gpu_step_with_logits, host_weights
+from helpers import calibrated_inv_tau, host_weights, run_teacher_forced
 from paper_2606_29094_amd import engine
 
 pytestmark = pytest.mark.gpu
@@ -39,52 +38,16 @@ def _model(cfg, t, inv_tau):
     return engine.DeviceModel(shape, t, inv_tau)
 
 
-def _calibrated_inv_tau(cfg, W, oreqs, mode):
-    """Calibrate on the oracle's first step of these requests (share 0.3 > 0.9)."""
-    zs = []
-    for oq in oreqs:
-        q = copy.deepcopy(oq)
-        h, rows, _ = oracle.step_forward(cfg, W, q, mode)
-        s, e = q.block_bounds
-        A = np.nonzero(q.mask[s:e])[0] + s
-        zs.append(oracle.head_logits(cfg, W, h[A - rows[0]], 1.0))
-    return float(oracle.calibrate(np.concatenate(zs), 0.9, 0.3)[1])
-
-
-def _run_teacher_forced(cfg, W, eng, reqs, oreqs, mode, inv_tau, n_steps):
-    """n_steps batched steps; before each, every request is set to the
-    oracle's state; each request's step is compared with the oracle's."""
-    stats = {"lerr": 0.0, "cerr": 0.0, "exempt": 0, "kinds": []}
-    for _ in range(n_steps):
-        active = [i for i, oq in enumerate(oreqs) if not oq.done]
-        if not active:
-            break
-        for i in active:
-            eng.set_state(reqs[i], oreqs[i].tokens, oreqs[i].mask, oreqs[i].k)
-        flags = [reqs[i].refreshed_block != reqs[i].block_start for i in active]
-        z_rows, out, starts = gpu_step_with_logits(eng, [reqs[i] for i in active])
-        for j, i in enumerate(active):
-            res = oracle.denoise_step(cfg, W, oreqs[i], mode, inv_tau, keep_logits=True)
-            assert res.refresh == (flags[j] or mode == "none")
-            stats["kinds"].append(res.refresh)
-            l, c, e = check_step_e2e(res, {k: v[j] for k, v in out.items()}, starts[j],
-                                     reqs[i].threshold, z_rows[j])
-            stats["lerr"] = max(stats["lerr"], l)
-            stats["cerr"] = max(stats["cerr"], c)
-            stats["exempt"] += e
-    return stats
-
-
 def test_mha_nocache_full_width(mha):
     """MHA shapes of the 256+256 no-cache workload (512 recomputed rows)."""
     cfg, t, W = mha
     prompt, G, thr = synth.request(synth.C2, 0)
     oreqs = [oracle.Request.new(prompt, G, 32, thr, cfg.mask_id)]
-    inv_tau = _calibrated_inv_tau(cfg, W, oreqs, "none")
+    inv_tau = calibrated_inv_tau(cfg, W, oreqs, "none")
     eng = engine.Engine(_model(cfg, t, inv_tau), 1, 512, "none")
     reqs = [engine.Request(prompt, G, 32, thr)]
     eng.admit(reqs[0], cfg.mask_id)
-    st = _run_teacher_forced(cfg, W, eng, reqs, oreqs, "none", inv_tau, 2)
+    st = run_teacher_forced(cfg, W, eng, reqs, oreqs, "none", inv_tau, 2)
     print("mha none:", st)
 
 
@@ -98,12 +61,12 @@ def test_mha_cache_steps_ragged_batch(mha, mode):
     gammas = [0.9, 0.7, 0.95]
     oreqs = [oracle.Request.new(p, g, 32, gm, cfg.mask_id)
              for p, (_, g), gm in zip(prompts, specs, gammas)]
-    inv_tau = _calibrated_inv_tau(cfg, W, oreqs, mode)
+    inv_tau = calibrated_inv_tau(cfg, W, oreqs, mode)
     eng = engine.Engine(_model(cfg, t, inv_tau), 3, 320, mode)
     reqs = [engine.Request(p, g, 32, gm) for p, (_, g), gm in zip(prompts, specs, gammas)]
     for r in reqs:
         eng.admit(r, cfg.mask_id)
-    st = _run_teacher_forced(cfg, W, eng, reqs, oreqs, mode, inv_tau, 4)
+    st = run_teacher_forced(cfg, W, eng, reqs, oreqs, mode, inv_tau, 4)
     print(mode, st)
     assert any(st["kinds"]) and not all(st["kinds"])
 
@@ -113,12 +76,12 @@ def test_gqa_dual_refresh_then_cache(gqa):
     cfg, t, W = gqa
     prompts = [synth.tokens(900 + i, 128, cfg.vocab) for i in range(2)]
     oreqs = [oracle.Request.new(p, 128, 64, 0.9, cfg.mask_id) for p in prompts]
-    inv_tau = _calibrated_inv_tau(cfg, W, oreqs, "dual")
+    inv_tau = calibrated_inv_tau(cfg, W, oreqs, "dual")
     eng = engine.Engine(_model(cfg, t, inv_tau), 2, 256, "dual")
     reqs = [engine.Request(p, 128, 64, 0.9) for p in prompts]
     for r in reqs:
         eng.admit(r, cfg.mask_id)
-    st = _run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 3)
+    st = run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 3)
     print("gqa dual:", st)
     assert st["kinds"][:2] == [True, True] and not all(st["kinds"])
 
@@ -129,18 +92,18 @@ def test_mixed_refresh_and_cache_in_one_batch(mha):
     cfg, t, W = mha
     prompts = [synth.tokens(700 + i, p, cfg.vocab) for i, p in enumerate((150, 60, 97))]
     oreqs = [oracle.Request.new(p, 64, 32, 0.8, cfg.mask_id) for p in prompts]
-    inv_tau = _calibrated_inv_tau(cfg, W, oreqs, "dual")
+    inv_tau = calibrated_inv_tau(cfg, W, oreqs, "dual")
     eng = engine.Engine(_model(cfg, t, inv_tau), 3, 256, "dual")
     reqs = [engine.Request(p, 64, 32, 0.8) for p in prompts]
     for r in reqs:
         eng.admit(r, cfg.mask_id)
-    _run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 1)
+    run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 1)
     # request 0 jumps to its second block (block 1 filled in), the others stay
     oq = oreqs[0]
     s, e = oq.block_bounds
     oq.tokens[s:e] = synth.tokens(77, e - s, cfg.vocab)
     oq.mask[s:e] = False
     oq.k += 1
-    st = _run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 1)
+    st = run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 1)
     assert st["kinds"] == [True, False, False]
     print("mixed:", st)
