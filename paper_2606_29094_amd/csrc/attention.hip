@@ -2,10 +2,17 @@
 // cached key/value position of their request's slot: O = softmax(Q K^T /
 // sqrt(dh)) V per query head; query head h reads key/value head h / (Hq/Hkv).
 //
-// bf16 path (matrix cores): one block = 32 or 64 query rows of one request x
-// one query head; waves split the rows in groups of 16 and the keys in two
-// groups (see attn_bf16_kernel). Key tiles are staged in LDS (keys row-major,
-// values transposed, which is how the cache stores them).
+// bf16 path (matrix cores), two kernels:
+//  * attn_gqa_kernel: one block = all query heads that share a key/value head
+//    (one for MHA) x 16-64 query rows of one request; 64-key tiles loaded
+//    directly into a two-stage LDS ring. Used for grouped-query attention and
+//    for MHA launches with at least two blocks per CU.
+//  * attn_bf16_kernel: one block = 32 or 64 query rows of one request x one
+//    query head; waves split the rows in groups of 16 and the keys in two
+//    groups, tiles staged through registers. Used for MHA launches with few
+//    blocks (one request's no-cache step, cache steps of short blocks).
+// Key tiles are staged in LDS keys row-major and values transposed, which is
+// how the cache stores them.
 // Each wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (keys as the A
 // operand, its 16 query rows as B, held in registers), so that every lane
 // ends up owning one query and 16 keys: the online softmax needs only two
@@ -300,10 +307,10 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
   }
 }
 
-// Grouped-query attention (GH > 1 query heads per key/value head): one block
-// = the GH query heads of one key/value head x QG groups of 16 query rows of
-// one request, one wave per (query head, row group), so every staged K/V
-// tile serves GH * QG * 16 query rows. Tiles of 64 keys are fetched with
+// Shared-tile kernel (GH query heads per key/value head; GH = 1 for MHA):
+// one block = the GH query heads of one key/value head x QG groups of 16
+// query rows of one request, one wave per (query head, row group), so every
+// staged K/V tile serves GH * QG * 16 query rows. Tiles of 64 keys are fetched with
 // direct global->LDS loads into a two-stage ring: the next tile's loads run
 // during the current tile's MFMAs and no registers hold tiles in flight,
 // which keeps the register count low enough for two blocks per CU.
@@ -633,8 +640,7 @@ static hipError_t launch_gqa(const StepPlan& p, const bf16* q, const bf16* kc, c
 }
 
 // Grouped-query attention with 2, 4, 7 or 8 query heads per key/value head:
-// the shared-tile kernel with 7 or 8 waves per block; other head ratios and
-// MHA use the per-head kernel.
+// the shared-tile kernel with 7 or 8 waves per block.
 template <int DH>
 static hipError_t attention_dh(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
                                int s_max, int hq, int hkv, bf16* out, float scale_log2,
@@ -646,10 +652,19 @@ static hipError_t attention_dh(const StepPlan& p, const bf16* q, const bf16* kc,
     case 8: return launch_gqa<DH, 8, 1, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
     default: break;
   }
-  // Query tiles of 32 rows when no request recomputes more than 32 rows
-  // (cache steps of blocks <= 32), else 64; two key groups either way.
-  int max_rows = 0;
-  for (int r = 0; r < p.n_req; ++r) max_rows = max(max_rows, p.r[r].nrows);
+  // MHA and other ratios. With at least two 64-row blocks per CU (256 CUs)
+  // the shared-tile kernel with one head per block (4 waves) is used: its
+  // blocks overlap each other's loads. Otherwise the per-head kernel with
+  // two key groups per block (8 waves), on query tiles of 32 rows when no
+  // request recomputes more than 32 rows (cache steps of blocks <= 32), else
+  // 64.
+  int max_rows = 0, tiles64 = 0;
+  for (int r = 0; r < p.n_req; ++r) {
+    max_rows = max(max_rows, p.r[r].nrows);
+    tiles64 += (p.r[r].nrows + 63) / 64;
+  }
+  if (hq == hkv && max_rows > 32 && (long)hq * tiles64 >= 512)
+    return launch_gqa<DH, 1, 4, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
   return max_rows <= 32
              ? launch_attn<DH, 2, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
              : launch_attn<DH, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
