@@ -204,18 +204,26 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
                                size_t ws_bytes, void* stream);
 
 /* Kernel timing. While enabled, every kernel the library enqueues for this
- * model (or, when only_class is not NULL, every kernel of that class) is
- * bracketed by a pair of HIP events on the launch stream. dlm_profile_read
- * waits for those events, adds their elapsed times per kernel class into
- * out[0 .. *n_out) (at most cap entries, in first-seen order) and clears them.
- * Each timed launch costs two event records on the host. */
+ * model (or, when only_class is not NULL, every kernel of that class; see also
+ * dlm_profile_sample) is bracketed by a pair of HIP events on the launch
+ * stream. dlm_profile_read waits for those events, adds their elapsed times
+ * per kernel class into out[0 .. *n_out) (at most cap entries, in first-seen
+ * order) and clears them. Each timed launch costs two event records on the
+ * host and a few microseconds of GPU idle time around the launch. */
 typedef struct dlm_profile_entry {
   char name[32];          /* kernel class, e.g. "gemm_gate_up_swiglu"                  */
   int32_t calls;          /* launches timed                                             */
   double total_ms;        /* sum of their event-to-event times                          */
+  int32_t launches;       /* launches of the class since the last read, timed or not    */
 } dlm_profile_entry;
 dlm_status dlm_profile_enable(dlm_model* m, int32_t on, const char* only_class);
 dlm_status dlm_profile_read(dlm_model* m, dlm_profile_entry* out, int32_t cap, int32_t* n_out);
+/* Time only the launches 0, every, 2 every, ... of each selected class (counted
+ * from the last dlm_profile_enable or dlm_profile_sample call); 1 (the
+ * default) times all. With every coprime to the layer count the timed
+ * launches rotate through the layers at about one event pair per step.
+ * DLM_EINVAL when every < 1. */
+dlm_status dlm_profile_sample(dlm_model* m, int32_t every);
 
 /* Measured ceilings (benchmark support, not part of the method). */
 /* dlm_ceiling_mfma: n_blocks blocks of 4 waves, each wave running iters x 32

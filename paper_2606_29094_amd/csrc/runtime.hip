@@ -64,7 +64,17 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 struct Profiler {
   bool on = false;
   std::string only;        // empty: every class
-  bool wants(const char* n) const { return on && (only.empty() || only == n); }
+  int every = 1;           // time one launch in `every` of each class
+  std::vector<long> seen;  // launches of each class since enable / sample (sampling phase)
+  std::vector<int> since_read;   // launches of each class since the last read
+  bool wants(const char* n) {
+    if (!on || !(only.empty() || only == n)) return false;
+    const int k = kind_of(n);
+    if ((int)seen.size() <= k) seen.resize(k + 1, 0);
+    if ((int)since_read.size() <= k) since_read.resize(k + 1, 0);
+    since_read[k] += 1;
+    return seen[k]++ % every == 0;
+  }
   struct Rec { int kind; hipEvent_t a, b; };
   std::vector<Rec> pending;
   std::vector<hipEvent_t> pool;
@@ -455,6 +465,16 @@ dlm_status dlm_profile_enable(dlm_model* m, int32_t on, const char* only_class) 
   if (!m) return fail(DLM_EINVAL, "model is NULL");
   m->prof.on = on != 0;
   m->prof.only = only_class ? only_class : "";
+  m->prof.seen.clear();
+  return DLM_OK;
+}
+
+dlm_status dlm_profile_sample(dlm_model* m, int32_t every) {
+  g_err.clear();
+  if (!m) return fail(DLM_EINVAL, "model is NULL");
+  if (every < 1) return fail(DLM_EINVAL, "every %d < 1", every);
+  m->prof.every = every;
+  m->prof.seen.clear();
   return DLM_OK;
 }
 
@@ -479,14 +499,17 @@ dlm_status dlm_profile_read(dlm_model* m, dlm_profile_entry* out, int32_t cap, i
   pf.pending.clear();
   int n = 0;
   for (size_t k = 0; k < pf.names.size(); ++k) {
-    if (calls[k] == 0) continue;
+    const int launches = k < pf.since_read.size() ? pf.since_read[k] : 0;
+    if (calls[k] == 0 && launches == 0) continue;
     if (n < cap) {
       snprintf(out[n].name, sizeof out[n].name, "%s", pf.names[k].c_str());
       out[n].calls = calls[k];
       out[n].total_ms = ms[k];
+      out[n].launches = launches;
     }
     ++n;
   }
+  pf.since_read.assign(pf.since_read.size(), 0);
   *n_out = n < cap ? n : cap;
   return st;
 }

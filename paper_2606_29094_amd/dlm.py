@@ -26,7 +26,7 @@ EXPORTS = ["dlm_load_weights", "dlm_model_destroy", "dlm_workspace_bytes",
            "dlm_kv_cache_alloc", "dlm_cache_destroy", "dlm_cache_invalidate",
            "dlm_denoise_step", "dlm_cache_refresh", "dlm_debug_logits",
            "dlm_head_confidence", "dlm_profile_enable", "dlm_profile_read",
-           "dlm_ceiling_mfma", "dlm_ceiling_copy", "dlm_last_error"]
+           "dlm_profile_sample", "dlm_ceiling_mfma", "dlm_ceiling_copy", "dlm_last_error"]
 
 
 class DlmConfig(ctypes.Structure):
@@ -64,7 +64,8 @@ class DlmStepOut(ctypes.Structure):
 
 
 class DlmProfileEntry(ctypes.Structure):
-    _fields_ = [("name", ctypes.c_char * 32), ("calls", c_int32), ("total_ms", ctypes.c_double)]
+    _fields_ = [("name", ctypes.c_char * 32), ("calls", c_int32), ("total_ms", ctypes.c_double),
+                ("launches", c_int32)]
 
 
 class DlmError(RuntimeError):
@@ -103,6 +104,7 @@ def lib():
         L.dlm_profile_enable.argtypes = [c_void_p, c_int32, ctypes.c_char_p]
         L.dlm_profile_read.argtypes = [c_void_p, POINTER(DlmProfileEntry), c_int32,
                                        POINTER(c_int32)]
+        L.dlm_profile_sample.argtypes = [c_void_p, c_int32]
         L.dlm_ceiling_mfma.argtypes = [c_int32, c_int32, c_void_p, POINTER(ctypes.c_double),
                                        c_void_p]
         L.dlm_ceiling_copy.argtypes = [c_void_p, c_void_p, c_size_t, c_void_p]
@@ -111,7 +113,7 @@ def lib():
         for name in ["dlm_load_weights", "dlm_workspace_bytes", "dlm_kv_cache_alloc",
                      "dlm_cache_invalidate", "dlm_denoise_step", "dlm_cache_refresh",
                      "dlm_debug_logits", "dlm_head_confidence", "dlm_profile_enable",
-                     "dlm_profile_read"]:
+                     "dlm_profile_read", "dlm_profile_sample"]:
             getattr(L, name).restype = c_int32
         _lib = L
     return _lib
@@ -217,12 +219,19 @@ def profile_enable(model, on: bool, only_class: str | None = None):
                                    None if only_class is None else only_class.encode()))
 
 
+def profile_sample(model, every: int):
+    """Time one launch in `every` of each selected class (1: all)."""
+    check(lib().dlm_profile_sample(model, every))
+
+
 def profile_read(model, cap: int = 64) -> dict:
-    """{kernel class: (calls, total ms)} of the launches timed since the last read."""
+    """{kernel class: (timed launches, their total ms, all launches)} since the
+    last read."""
     arr = (DlmProfileEntry * cap)()
     n = c_int32()
     check(lib().dlm_profile_read(model, arr, cap, ctypes.byref(n)))
-    return {arr[i].name.decode(): (arr[i].calls, arr[i].total_ms) for i in range(n.value)}
+    return {arr[i].name.decode(): (arr[i].calls, arr[i].total_ms, arr[i].launches)
+            for i in range(n.value)}
 
 
 def ceiling_mfma(n_blocks: int, iters: int, out_ptr: int, stream: int) -> float:

@@ -188,3 +188,21 @@ def test_engine_request_block_bookkeeping():
     assert not r.done
     r.k = 3
     assert r.done
+
+
+def test_profile_sample_validation():
+    _lib_or_skip()
+    m = _load()
+    try:
+        dlm.profile_sample(m, 1)
+        dlm.profile_sample(m, 31)
+        with pytest.raises(dlm.DlmError) as e:
+            dlm.profile_sample(m, 0)
+        assert e.value.status == dlm.DLM_EINVAL and "every" in dlm.last_error()
+        dlm.profile_enable(m, True, "gemm_gate_up_swiglu")
+        assert dlm.profile_read(m) == {}
+        dlm.profile_enable(m, False)
+    finally:
+        dlm.model_destroy(m)
+    with pytest.raises(dlm.DlmError):
+        dlm.profile_sample(None, 2)
