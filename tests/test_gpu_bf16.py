@@ -12,7 +12,7 @@ import pytest
 import oracle
 import synth
 import synth.device as sdev
-from helpers import calibrated_inv_tau, host_weights, run_teacher_forced
+from helpers import calibrated_inv_tau, gpu_step_with_logits, host_weights, run_teacher_forced
 from paper_2606_29094_amd import engine
 
 pytestmark = pytest.mark.gpu
@@ -107,3 +107,23 @@ def test_mixed_refresh_and_cache_in_one_batch(mha):
     st = run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 1)
     assert st["kinds"] == [True, False, False]
     print("mixed:", st)
+
+
+def test_mha_nocache_step_is_bitwise_repeatable(mha):
+    """The 512-row no-cache step twice from the same state: logits and
+    confidences identical bit for bit (no atomics in the arithmetic: split-K
+    slices are summed in slice order by their consumer)."""
+    cfg, t, W = mha
+    prompt, G, thr = synth.request(synth.C2, 0)
+    model = _model(cfg, t, 8.0)
+    runs = []
+    for _ in range(2):
+        eng = engine.Engine(model, 1, 512, "none")
+        r = engine.Request(prompt, G, 32, thr)
+        eng.admit(r, cfg.mask_id)
+        z, out, _ = gpu_step_with_logits(eng, [r])
+        runs.append((z[0].copy(), out["block_conf"].copy(), out["pos"].copy()))
+        eng.close()
+    model.close()
+    for a, b in zip(runs[0], runs[1]):
+        assert np.array_equal(a, b)
