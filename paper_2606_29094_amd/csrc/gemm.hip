@@ -180,7 +180,8 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // max(0.7, fill) of a full one. When K is split, the fp32 slices add their HBM
 // traffic (written by the GEMM, read back by the consumer). The cheapest
 // (configuration, split) wins. 128x192 with two blocks per CU (cfg 22) runs
-// without K splits only; the small tiles only for few rows.
+// without K splits only (its table holds unsplit launches); the small tiles
+// only for few rows.
 namespace {
 struct RoundTable {
   int cfg, occ, max_m;
@@ -238,11 +239,11 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
   }
   double best_t = 1e30;
   for (const RoundTable& c : kRoundTables) {
-    if (M > c.max_m || (c.unsplit_only && splittable)) continue;
+    if (M > c.max_m) continue;
     int bm, bn, th;
     gemm_dl_tile(c.cfg, &bm, &bn, &th);
     for (int s = 1; s <= 8; s *= 2) {
-      if (s > 1 && (!splittable || (K / 64) % s != 0 || K / s < 512)) continue;
+      if (s > 1 && (c.unsplit_only || !splittable || (K / 64) % s != 0 || K / s < 512)) continue;
       const long units = (long)ceil_div(M, bm) * ceil_div(N, bn) * s;
       const long slots = (long)num_cu * c.occ;
       const long full = units / slots;

@@ -79,6 +79,9 @@ struct EpiScaledStore {
   }
 };
 
+// C += acc (the residual update). The loads of one 16-row fragment row are all
+// issued before its stores: element by element, each load would wait for the
+// previous store (the compiler cannot tell that the addresses differ).
 struct EpiAdd {
   float* C; int ldc; int M, N;
   __device__ int b_row(int n) const { return n; }
@@ -87,17 +90,27 @@ struct EpiAdd {
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int, int, int, int) const {
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
+    for (int fm = 0; fm < FM; ++fm) {
+      float cv[4][FN];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
-        if (m >= M) continue;
+        const int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) {
-          int n = n0 + fn * 16 + (lane & 15);
-          if (n < N) C[(long)m * ldc + n] += acc[fm][fn][i];
+          const int n = n0 + fn * 16 + (lane & 15);
+          cv[i][fn] = m < M && n < N ? C[(long)m * ldc + n] : 0.f;
         }
       }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          const int n = n0 + fn * 16 + (lane & 15);
+          if (m < M && n < N) C[(long)m * ldc + n] = cv[i][fn] + acc[fm][fn][i];
+        }
+      }
+    }
   }
 };
 
