@@ -173,32 +173,41 @@ struct EpiLMHead {
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int wave_n,
                              char* smem, int waves_n, int bm, int block_m0,
                              int tile_n, int) const {
-    // stats per (fm, i) row for this lane over its FN columns
+    // per row (fm, i) over the wave's columns: each lane takes the max and its
+    // lowest column over its FN columns; the 16 lanes that hold the row agree
+    // on the row max, sum exp(z - max) with one exp per element, and take the
+    // lowest column among the lanes that reached the max
     RowStat st[FM][4];
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        RowStat r = {-INFINITY, 0.f, 0x7fffffff};
+        float mx = -INFINITY;
+        int ix = 0x7fffffff;
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) {
-          int n = n0 + fn * 16 + (lane & 15);
-          if (n < V) {
-            float z = acc[fm][fn][i] * inv_tau;
-            RowStat c = {z, 1.f, n};
-            r = combine(r, c);
+          const int n = n0 + fn * 16 + (lane & 15);
+          const float z = acc[fm][fn][i] * inv_tau;
+          if (n < V && z > mx) { mx = z; ix = n; }   // columns ascend with fn: ties keep the lowest
+        }
+        float gm = mx;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) gm = fmaxf(gm, __shfl_xor(gm, o, 64));
+        float s = 0.f;
+        if (gm != -INFINITY) {
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn) {
+            const int n = n0 + fn * 16 + (lane & 15);
+            if (n < V) s += __expf(acc[fm][fn][i] * inv_tau - gm);
           }
         }
-        // across the 16 lanes that hold the other columns of these rows
+        int gi = mx == gm ? ix : 0x7fffffff;
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) {
-          RowStat x;
-          x.m = __shfl_xor(r.m, o, 64);
-          x.s = __shfl_xor(r.s, o, 64);
-          x.i = __shfl_xor(r.i, o, 64);
-          r = combine(r, x);
+          s += __shfl_xor(s, o, 64);
+          gi = min(gi, __shfl_xor(gi, o, 64));
         }
-        st[fm][i] = r;
+        st[fm][i] = RowStat{gm, s, gi};
       }
     // across the waves that share these rows (different column ranges): LDS
     RowStat* buf = reinterpret_cast<RowStat*>(smem);
