@@ -27,6 +27,18 @@ template <> struct MfmaTraits<float> {
 constexpr int kRowBytes = 128;          // k-tile bytes per row
 constexpr int kLdsRow = kRowBytes + 16; // padded LDS row stride
 
+// two adjacent outputs in one store (4 bytes for bf16, 8 for fp32)
+__device__ __forceinline__ void store2(float* o, float a, float b) {
+  *reinterpret_cast<float2*>(o) = make_float2(a, b);
+}
+__device__ __forceinline__ void store2(bf16* o, float a, float b) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v;
+  v[0] = (bf16)a;
+  v[1] = (bf16)b;
+  *reinterpret_cast<bf16x2*>(o) = v;
+}
+
 // ------------------------------------------------------------ epilogues --
 // Each epilogue sees the wave's accumulators: acc[fm][fn][i] is the value at
 // row m0 + fm*16 + 4*(lane/16) + i, column n0 + fn*16 + lane%16. The further
@@ -125,24 +137,35 @@ struct EpiSwiGLU {
     return ((n >> 4) & 1) ? F + f : f;
   }
   __device__ bool skip_tile(int) const { return false; }
+  // silu(g) * u with silu(g) = g / (1 + exp(-g)) through the hardware
+  // reciprocal (about 1 ulp; the result is rounded to the storage type).
+  // Outputs go out in pairs of adjacent columns: for rows i and i + 1 of a
+  // fragment, lane 2k and lane 2k + 1 swap one value each, then lane 2k
+  // stores columns (f, f + 1) of row i and lane 2k + 1 those of row i + 1.
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int, int, int, int) const {
     static_assert(FN % 2 == 0, "gate/up pairs");
+    const bool odd = lane & 1;
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int m = m0 + fm * 16 + 4 * (lane >> 4) + i;
-        if (m >= M) continue;
+      for (int i = 0; i < 4; i += 2) {
+        const int m = m0 + fm * 16 + 4 * (lane >> 4) + i + (odd ? 1 : 0);   // row this lane stores
 #pragma unroll
         for (int fn = 0; fn < FN; fn += 2) {
-          int n = n0 + fn * 16;               // multiple of 32
-          int f = (n >> 5) * 16 + (lane & 15);
-          if (f >= F) continue;
-          float g = acc[fm][fn][i], u = acc[fm][fn + 1][i];
-          float s = g / (1.0f + __expf(-g));
-          out[(long)m * ldo + f] = from_f32<T>(s * u);
+          float y[2];
+#pragma unroll
+          for (int k = 0; k < 2; ++k) {
+            const float g = acc[fm][fn][i + k], u = acc[fm][fn + 1][i + k];
+            y[k] = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+          }
+          const float recv = __shfl_xor(odd ? y[0] : y[1], 1, 64);
+          const int f = (((n0 + fn * 16) >> 5) * 16) + ((lane & 15) & ~1);   // even column
+          if (m < M && f < F) {
+            const float lo = odd ? recv : y[0], hi = odd ? y[1] : recv;
+            store2(out + (long)m * ldo + f, lo, hi);
+          }
         }
       }
   }
