@@ -207,8 +207,11 @@ hipError_t rope_table(const StepPlan& p, int head_dim, float theta, float2* cs, 
 //   y >= hq         : kv head y - hq -> rotated key to K[slot][j][pos][:],
 //                                       value (transposed in LDS) to V[slot][j][:][pos]
 // The fp32 input is the sum of the split-K partial slices of the QKV GEMM.
-template <typename T, int DH>
-__global__ __launch_bounds__(256) void qkv_rope_scatter_kernel(
+// NTH threads per block: 1024 (one pass over the tile) when the launch has few
+// blocks, so that each CU keeps more loads in flight; 256 (four quads per
+// thread per pass) when it has many.
+template <typename T, int DH, int NTH>
+__global__ __launch_bounds__(NTH) void qkv_rope_scatter_kernel(
     StepPlan p, const float* __restrict__ qkv, int splits, long split_stride,
     const float2* __restrict__ cs, int hq, int hkv, T* __restrict__ q_out,
     T* __restrict__ kcache, T* __restrict__ vcache, int s_max) {
@@ -225,28 +228,52 @@ __global__ __launch_bounds__(256) void qkv_rope_scatter_kernel(
   const int pos_base = q.pos0 + lrow0;
 
 
-  // rotary pairs (i, i + HALF): each thread takes 4 consecutive i of one row
+  // rotary pairs (i, i + HALF): each thread takes 4 consecutive i of one row,
+  // UNR such quads per pass (a 64-row tile in one pass) with all their loads
+  // issued before the stores
   auto rotate = [&](int col0, T* dst_base, long dst_row_stride, bool kv) {
-    constexpr int QUADS = HALF / 4;
-    for (int idx = threadIdx.x; idx < nvalid * QUADS; idx += blockDim.x) {
-      const int rr = idx / QUADS, i = (idx % QUADS) * 4;
-      const int n = row_base + rr;
-      const float* src = qkv + (long)n * qkv_dim + col0 + i;
-      float4 a = *reinterpret_cast<const float4*>(src);
-      float4 b = *reinterpret_cast<const float4*>(src + HALF);
-      for (int sp = 1; sp < splits; ++sp) {
-        const float4 a2 = *reinterpret_cast<const float4*>(src + sp * split_stride);
-        const float4 b2 = *reinterpret_cast<const float4*>(src + sp * split_stride + HALF);
-        a.x += a2.x; a.y += a2.y; a.z += a2.z; a.w += a2.w;
-        b.x += b2.x; b.y += b2.y; b.z += b2.z; b.w += b2.w;
+    constexpr int QUADS = HALF / 4, UNR = (kQTile * QUADS + NTH - 1) / NTH;
+    const int total = nvalid * QUADS;
+    for (int base = threadIdx.x; base < total; base += UNR * blockDim.x) {
+      float4 a[UNR], b[UNR], c01[UNR], c23[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int idx = base + u * blockDim.x;
+        if (idx >= total) break;
+        const int rr = idx / QUADS, i = (idx % QUADS) * 4;
+        const int n = row_base + rr;
+        const float* src = qkv + (long)n * qkv_dim + col0 + i;
+        a[u] = *reinterpret_cast<const float4*>(src);
+        b[u] = *reinterpret_cast<const float4*>(src + HALF);
+        c01[u] = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i);
+        c23[u] = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i + 2);
       }
-      const float4 c01 = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i);
-      const float4 c23 = *reinterpret_cast<const float4*>(cs + (long)n * HALF + i + 2);
-      T* o = dst_base + (kv ? (long)(pos_base + rr) : (long)n) * dst_row_stride;
-      store4(o + i, a.x * c01.x - b.x * c01.y, a.y * c01.z - b.y * c01.w,
-             a.z * c23.x - b.z * c23.y, a.w * c23.z - b.w * c23.w);
-      store4(o + i + HALF, b.x * c01.x + a.x * c01.y, b.y * c01.z + a.y * c01.w,
-             b.z * c23.x + a.z * c23.y, b.w * c23.z + a.w * c23.w);
+      for (int sp = 1; sp < splits; ++sp) {
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int idx = base + u * blockDim.x;
+          if (idx >= total) break;
+          const int rr = idx / QUADS, i = (idx % QUADS) * 4;
+          const float* src = qkv + (long)(row_base + rr) * qkv_dim + col0 + i + sp * split_stride;
+          const float4 a2 = *reinterpret_cast<const float4*>(src);
+          const float4 b2 = *reinterpret_cast<const float4*>(src + HALF);
+          a[u].x += a2.x; a[u].y += a2.y; a[u].z += a2.z; a[u].w += a2.w;
+          b[u].x += b2.x; b[u].y += b2.y; b[u].z += b2.z; b[u].w += b2.w;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int idx = base + u * blockDim.x;
+        if (idx >= total) break;
+        const int rr = idx / QUADS, i = (idx % QUADS) * 4;
+        const int n = row_base + rr;
+        T* o = dst_base + (kv ? (long)(pos_base + rr) : (long)n) * dst_row_stride;
+        store4(o + i, a[u].x * c01[u].x - b[u].x * c01[u].y, a[u].y * c01[u].z - b[u].y * c01[u].w,
+               a[u].z * c23[u].x - b[u].z * c23[u].y, a[u].w * c23[u].z - b[u].w * c23[u].w);
+        store4(o + i + HALF, b[u].x * c01[u].x + a[u].x * c01[u].y,
+               b[u].y * c01[u].z + a[u].y * c01[u].w, b[u].z * c23[u].x + a[u].z * c23[u].y,
+               b[u].w * c23[u].z + a[u].w * c23[u].w);
+      }
     }
   };
   if (y < hq) {
@@ -259,18 +286,40 @@ __global__ __launch_bounds__(256) void qkv_rope_scatter_kernel(
   const int kcol = hq * DH + j * DH;
   const int vcol = (hq + hkv) * DH + j * DH;
   rotate(kcol, kb, DH, true);
-  for (int idx = threadIdx.x; idx < nvalid * (DH / 4); idx += blockDim.x) {
-    const int rr = idx / (DH / 4), d = (idx % (DH / 4)) * 4;
-    const float* src = qkv + (long)(row_base + rr) * qkv_dim + vcol + d;
-    float4 v = *reinterpret_cast<const float4*>(src);
-    for (int sp = 1; sp < splits; ++sp) {
-      const float4 v2 = *reinterpret_cast<const float4*>(src + sp * split_stride);
-      v.x += v2.x; v.y += v2.y; v.z += v2.z; v.w += v2.w;
+  {
+    constexpr int UNR = (kQTile * (DH / 4) + NTH - 1) / NTH;
+    const int total = nvalid * (DH / 4);
+    for (int base = threadIdx.x; base < total; base += UNR * blockDim.x) {
+      float4 v[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int idx = base + u * blockDim.x;
+        if (idx >= total) break;
+        const int rr = idx / (DH / 4), d = (idx % (DH / 4)) * 4;
+        v[u] = *reinterpret_cast<const float4*>(qkv + (long)(row_base + rr) * qkv_dim + vcol + d);
+      }
+      for (int sp = 1; sp < splits; ++sp) {
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int idx = base + u * blockDim.x;
+          if (idx >= total) break;
+          const int rr = idx / (DH / 4), d = (idx % (DH / 4)) * 4;
+          const float4 v2 = *reinterpret_cast<const float4*>(
+              qkv + (long)(row_base + rr) * qkv_dim + vcol + d + sp * split_stride);
+          v[u].x += v2.x; v[u].y += v2.y; v[u].z += v2.z; v[u].w += v2.w;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int idx = base + u * blockDim.x;
+        if (idx >= total) break;
+        const int rr = idx / (DH / 4), d = (idx % (DH / 4)) * 4;
+        vt[d + 0][rr] = from_f32<T>(v[u].x);
+        vt[d + 1][rr] = from_f32<T>(v[u].y);
+        vt[d + 2][rr] = from_f32<T>(v[u].z);
+        vt[d + 3][rr] = from_f32<T>(v[u].w);
+      }
     }
-    vt[d + 0][rr] = from_f32<T>(v.x);
-    vt[d + 1][rr] = from_f32<T>(v.y);
-    vt[d + 2][rr] = from_f32<T>(v.z);
-    vt[d + 3][rr] = from_f32<T>(v.w);
   }
   __syncthreads();
   for (int idx = threadIdx.x; idx < nvalid * DH; idx += blockDim.x) {
@@ -285,14 +334,18 @@ hipError_t qkv_rope_scatter(const StepPlan& p, const float* qkv, int splits, lon
                             T* kcache, T* vcache, int s_max, hipStream_t st) {
   if (p.n_tiles == 0) return hipSuccess;
   dim3 g(p.n_tiles, hq + hkv);
-  if (dh == 128)
-    hipLaunchKernelGGL((qkv_rope_scatter_kernel<T, 128>), g, dim3(256), 0, st, p, qkv, splits,
-                       split_stride, cs, hq, hkv, q_out, kcache, vcache, s_max);
-  else if (dh == 64)
-    hipLaunchKernelGGL((qkv_rope_scatter_kernel<T, 64>), g, dim3(256), 0, st, p, qkv, splits,
-                       split_stride, cs, hq, hkv, q_out, kcache, vcache, s_max);
-  else
+  const bool many = (long)p.n_tiles * (hq + hkv) >= 1024;   // four or more blocks per CU
+#define ROPE_LAUNCH(DH_, NTH_)                                                                   \
+  hipLaunchKernelGGL((qkv_rope_scatter_kernel<T, DH_, NTH_>), g, dim3(NTH_), 0, st, p, qkv,     \
+                     splits, split_stride, cs, hq, hkv, q_out, kcache, vcache, s_max)
+  if (dh == 128) {
+    if (many) ROPE_LAUNCH(128, 256); else ROPE_LAUNCH(128, 1024);
+  } else if (dh == 64) {
+    if (many) ROPE_LAUNCH(64, 256); else ROPE_LAUNCH(64, 1024);
+  } else {
     return hipErrorInvalidValue;
+  }
+#undef ROPE_LAUNCH
   return hipGetLastError();
 }
 
