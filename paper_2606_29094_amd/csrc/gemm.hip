@@ -267,6 +267,18 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
   return best;
 }
 
+// The LM head at <= 64 rows streams the vocab matrix once and is bound by HBM,
+// not by the round-time tables: measured with the rotated K walk, a weight row
+// pitch that is a multiple of 8 KB (the 4096-wide MHA head) runs best with the
+// 3-stage 64x128 tiles (two weight tiles in flight per block, 5.9 TB/s), other
+// pitches (the 3584-wide GQA head) with the 2-stage ones (three blocks per CU,
+// 5.8 TB/s).
+GemmPlan lm_head_plan(int es, int M, int V, int K, int num_cu) {
+  GemmPlan p = gemm_plan(es, M, V, K, false, num_cu);
+  if (p.cfg >= 0 && M <= 64) p = GemmPlan{((long)K * es) % 8192 == 0 ? 11 : 10, 1, 0};
+  return p;
+}
+
 template <typename T>
 hipError_t gemm_store_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
                           int N, int K, float* C, int ldc, hipStream_t st) {

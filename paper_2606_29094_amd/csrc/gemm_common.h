@@ -48,6 +48,7 @@ __device__ __forceinline__ void store2(bf16* o, float a, float b) {
 
 struct EpiStore {
   float* C; int ldc; long split_stride; int M, N;
+  static constexpr bool kRotateK = false;
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
@@ -71,6 +72,7 @@ struct EpiStore {
 
 struct EpiScaledStore {
   float* C; int ldc; int M, N; float scale;
+  static constexpr bool kRotateK = false;
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
@@ -96,6 +98,7 @@ struct EpiScaledStore {
 // previous store (the compiler cannot tell that the addresses differ).
 struct EpiAdd {
   float* C; int ldc; int M, N;
+  static constexpr bool kRotateK = false;
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
@@ -137,6 +140,7 @@ struct EpiSwiGLU {
     return ((n >> 4) & 1) ? F + f : f;
   }
   __device__ bool skip_tile(int) const { return false; }
+  static constexpr bool kRotateK = false;
   // silu(g) * u with silu(g) = g / (1 + exp(-g)) through the hardware
   // reciprocal (about 1 ulp; the result is rounded to the storage type).
   // Outputs go out in pairs of adjacent columns: for rows i and i + 1 of a
@@ -190,6 +194,7 @@ __device__ __forceinline__ RowStat combine(RowStat a, RowStat b) {
 struct EpiLMHead {
   float* pm; float* ps; int* pi; int M; int V; float inv_tau; int ld;  // ld = rows stride
   const int* m_count;
+  static constexpr bool kRotateK = true;   // weight streaming: rotate the K walk per column tile
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int m0) const { return m_count && m0 >= *m_count; }
   template <int FM, int FN>

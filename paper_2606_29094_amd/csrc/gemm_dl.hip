@@ -72,6 +72,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   const int kbeg = tz * k_per_split;
   const int kend = min(K, kbeg + k_per_split);
   const int nkt = kend > kbeg ? (kend - kbeg) / BK : 0;
+  // K order: epilogues that ask for it (the LM head, which streams a large
+  // weight matrix with a 2^n-byte row pitch) start each column tile's K walk
+  // at a different k-tile (column tile mod k-tiles), so that the blocks in
+  // flight read different column offsets of their weight rows at any moment
+  // and spread over the HBM channels (MHA vocab head with 32 rows: 4.5 -> 5.9
+  // TB/s); the others walk K from the start.
+  const int krot = Epi::kRotateK && nkt > 0 ? tn % nkt : 0;
+  auto ktile = [&](int kt) { const int k = kt + krot; return k >= nkt ? k - nkt : k; };
 
   // LDS chunk slot of global chunk c in row r: c ^ swz(r); 8 consecutive rows
   // (two per 128-byte bank line for 64-byte rows) map to distinct banks.
@@ -191,8 +199,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   // when SB >= 3 (vmcnt counts this wave's loads in issue order).
 #pragma unroll
   for (int t = 0; t < SB - 1; ++t)
-    if (t < nkt) issue_b(t, t);
-  if (nkt > 0) issue_a(0, 0);
+    if (t < nkt) issue_b(t, ktile(t));
+  if (nkt > 0) issue_a(0, ktile(0));
 
   for (int kt = 0; kt < nkt; ++kt) {
     if constexpr (SB >= 3) {
@@ -205,8 +213,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     // __syncthreads() would add a fence that drains every load in flight.
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if (kt + 1 < nkt) issue_a((kt + 1) & 1, kt + 1);
-    if (kt + SB - 1 < nkt) issue_b((kt + SB - 1) % SB, kt + SB - 1);
+    if (kt + 1 < nkt) issue_a((kt + 1) & 1, ktile(kt + 1));
+    if (kt + SB - 1 < nkt) issue_b((kt + SB - 1) % SB, ktile(kt + SB - 1));
     compute(kt & 1, kt % SB);
   }
   __syncthreads();
@@ -218,6 +226,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   X(1, 128, 128, 2, 2, 2, 128)   \
   X(6, 256, 256, 2, 4, 2, 128)   \
   X(10, 64, 128, 2, 2, 2, 128)   \
+  X(11, 64, 128, 2, 2, 3, 128)   \
   X(21, 256, 192, 4, 2, 2, 128)  \
   X(22, 128, 192, 2, 2, 2, 128)  \
   X(29, 256, 128, 4, 2, 3, 128)  \

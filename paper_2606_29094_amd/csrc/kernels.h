@@ -51,6 +51,8 @@ __device__ __forceinline__ int plan_req_of_tile(const StepPlan& p, int tile) {
 // kernel. splits: number of K slices (fp32 partial slices, summed by the consumer).
 struct GemmPlan { int cfg; int splits; int group_m; };   // group_m: tile order (0 = plain)
 GemmPlan gemm_plan(int elem_bytes, int M, int N, int K, bool splittable, int num_cu);
+// plan of the LM-head GEMM (M rows x V vocab entries)
+GemmPlan lm_head_plan(int elem_bytes, int M, int V, int K, int num_cu);
 template <typename T>
 hipError_t gemm_store_f32(const GemmPlan& p, const T* A, int lda, const T* B, int ldb, int M,
                           int N, int K, float* C, int ldc, hipStream_t st);

@@ -150,7 +150,7 @@ Layout layout(const dlm_model* m, int n, int n_req) {
   L.g_gu = gemm_plan(es_i, n, 2 * c.d_ffn, c.d_model, false, m->num_cu);
   L.g_down = gemm_plan(es_i, n, c.d_model, c.d_ffn, true, m->num_cu);
   L.m_max = std::min(n, n_req * kMaxBlock);
-  L.g_lm = gemm_plan(es_i, L.m_max, c.vocab, c.d_model, false, m->num_cu);
+  L.g_lm = lm_head_plan(es_i, L.m_max, c.vocab, c.d_model, m->num_cu);
   L.g_logits = L.g_lm;
   L.s_qkv = L.g_qkv.splits;
   L.s_o = L.g_o.splits;
@@ -636,7 +636,7 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
   if (!workspace) return fail(DLM_EINVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
     return fail(DLM_EINVAL, "workspace is not 256-byte aligned");
-  const GemmPlan gp = gemm_plan((int)m->es, m_rows, m->cfg.vocab, m->cfg.d_model, false, m->num_cu);
+  const GemmPlan gp = lm_head_plan((int)m->es, m_rows, m->cfg.vocab, m->cfg.d_model, m->num_cu);
   const int tiles = lm_head_tiles(gp, m->cfg.vocab);
   const size_t stat = align_up((size_t)tiles * m_rows * 4, 256);
   const size_t need = 3 * stat + 256;
