@@ -270,6 +270,9 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 10 device-to-device copies of MIB MiB (calibrates the "
                          "HBM byte counters) and exit")
+    ap.add_argument("--sample-every", type=int, default=0,
+                    help="time one launch in this many of the dominant kernel in the timed "
+                         "steps (default 3: a third of the layers, rotating)")
     ap.add_argument("--profile-steps", type=int, default=10,
                     help="untimed steps after the warm-up with every kernel class timed "
                          "(per-class breakdown, choice of the dominant kernel)")
@@ -378,7 +381,9 @@ def main():
             a[0] += f
             a[1] += bb
 
-    def one_step(account):
+    prof_work = {}                        # class -> [flops, bytes] over the profile steps
+
+    def one_step(account, prof_acc=None):
         for b in range(B):
             if slots[b].done:
                 if account:
@@ -394,6 +399,11 @@ def main():
         eng.enqueue_step(slots)
         if account:                       # host bookkeeping while the GPU runs the step
             account_step(rows, m, refresh)
+        if prof_acc is not None:
+            for k, (f, bb) in class_work(shape, rows, m).items():
+                a = prof_acc.setdefault(k, [0.0, 0.0])
+                a[0] += f
+                a[1] += bb
         counts = eng.finish_step(slots)   # read-back of the counts (synchronises)
         dt = time.perf_counter() - ts
         if account:
@@ -409,11 +419,11 @@ def main():
             stats["unmasked"] += sum(counts)
 
     # warm-up (untimed), then untimed profile steps with every kernel class
-    # bracketed by events (the per-class breakdown of the steady state and the
-    # dominant class); the timed steps then bracket only every (n_layers - 1)-th
-    # launch of the dominant class (about one per step, rotating through the
-    # layers): an event pair costs about 6 us of GPU idle time around the
-    # launch, which on every launch would add ~4 % to the timed steps
+    # timed (the per-class breakdown of the steady state and the dominant
+    # class); the timed steps then time every third launch of the dominant
+    # class (rotating through the layers). A timed launch carries its two
+    # events in its own dispatch (no extra stream commands); timing every
+    # launch still cost ~1 % of the step
     for _ in range(args.warmup):
         one_step(False)
     torch.cuda.synchronize()
@@ -422,7 +432,7 @@ def main():
     if not args.no_profile:
         dlm.profile_enable(model.handle, True)
         for _ in range(args.profile_steps):
-            one_step(False)
+            one_step(False, prof_work)
         torch.cuda.synchronize()
         dlm.profile_enable(model.handle, False)
         warm_prof = dlm.profile_read(model.handle)
@@ -430,7 +440,8 @@ def main():
                                                    "gemm_down", "attention", "lm_head")]
         if timed_cls:
             dom = max(timed_cls, key=lambda k: warm_prof[k][1])
-            dlm.profile_sample(model.handle, max(1, shape.n_layers - 1))
+            every = args.sample_every if args.sample_every > 0 else 3
+            dlm.profile_sample(model.handle, every)
             dlm.profile_enable(model.handle, True, dom)
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -452,6 +463,14 @@ def main():
     for name, (calls, tot, _) in warm_prof.items():
         kernels[name] = {"calls": calls, "avg_us": 1e3 * tot / max(calls, 1),
                          "share_of_kernel_time": tot / warm_total}
+        if name in prof_work and calls > 0 and tot > 0:
+            # achieved rates of the profile steps: the class's algorithmic work
+            # over those steps / its summed event time
+            f, bb = prof_work[name]
+            kernels[name].update({"tflops": f / (tot * 1e-3) / 1e12,
+                                  "gbs": bb / (tot * 1e-3) / 1e9,
+                                  "frac_mfma": f / (tot * 1e-3) / (peak * 1e12),
+                                  "frac_hbm": bb / (tot * 1e-3) / (PEAK_HBM_GBS * 1e9)})
     roof = None
     if dom is not None and dom in prof and dom in stats["cls"]:
         calls, tot, launches = prof[dom]              # timed launches, their ms, all launches

@@ -621,7 +621,7 @@ static hipError_t launch_attn(const StepPlan& p, const bf16* q, const bf16* kc, 
   int tiles = 0;
   for (int r = 0; r < p.n_req; ++r) tiles += (p.r[r].nrows + QT - 1) / QT;
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_bf16_kernel<DH, QG, KG, PLO>), dim3(hq, tiles), dim3(QG * KG * 64), 0, st,
+  DLM_LAUNCH((attn_bf16_kernel<DH, QG, KG, PLO>), dim3(hq, tiles), dim3(QG * KG * 64), 0, st,
                      p, q, kc, vc, s_max, hq, hkv, out, scale_log2);
   return hipGetLastError();
 }
@@ -634,7 +634,7 @@ static hipError_t launch_gqa(const StepPlan& p, const bf16* q, const bf16* kc, c
   int tiles = 0;
   for (int r = 0; r < p.n_req; ++r) tiles += (p.r[r].nrows + QT - 1) / QT;
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_gqa_kernel<DH, GH, QG, PLO>), dim3(hkv * tiles), dim3(GH * QG * 64), 0,
+  DLM_LAUNCH((attn_gqa_kernel<DH, GH, QG, PLO>), dim3(hkv * tiles), dim3(GH * QG * 64), 0,
                      st, p, q, kc, vc, s_max, hq, hkv, tiles, out, scale_log2);
   return hipGetLastError();
 }
@@ -687,10 +687,10 @@ hipError_t attention<float>(const StepPlan& p, const float* q, const float* kc, 
   const float scale = 1.0f / sqrtf((float)dh);
   dim3 g(p.n_tiles, hq);
   if (dh == 64)
-    hipLaunchKernelGGL(attn_f32_kernel<64>, g, dim3(64), 0, st, p, q, kc, vc, s_max, hq, hkv,
+    DLM_LAUNCH(attn_f32_kernel<64>, g, dim3(64), 0, st, p, q, kc, vc, s_max, hq, hkv,
                        out, scale);
   else if (dh == 128)
-    hipLaunchKernelGGL(attn_f32_kernel<128>, g, dim3(64), 0, st, p, q, kc, vc, s_max, hq, hkv,
+    DLM_LAUNCH(attn_f32_kernel<128>, g, dim3(64), 0, st, p, q, kc, vc, s_max, hq, hkv,
                        out, scale);
   else
     return hipErrorInvalidValue;

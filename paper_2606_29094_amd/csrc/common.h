@@ -2,6 +2,7 @@
 // conversion, MFMA fragment types and wavefront reductions.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -49,6 +50,25 @@ __device__ __forceinline__ f32x4 mfma16_f32(float a, float b, const f32x4& c) {
 }
 
 __host__ __device__ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// ---- kernel launches ----
+// Timing hook of the library's profiler: when the host sets start/stop (one
+// launch at a time), the next kernel launched through DLM_LAUNCH carries the
+// two events in its own dispatch, so they time the kernel itself (no extra
+// commands in the stream), and the hook is cleared.
+struct LaunchTiming { hipEvent_t start = nullptr, stop = nullptr; };
+extern thread_local LaunchTiming g_launch_timing;
+#define DLM_LAUNCH(kernel, grid, block, shmem, stream, ...)                                     \
+  do {                                                                                         \
+    if (::dlm::g_launch_timing.start) {                                                        \
+      const ::dlm::LaunchTiming lt_ = ::dlm::g_launch_timing;                                  \
+      ::dlm::g_launch_timing = ::dlm::LaunchTiming{};                                          \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, lt_.start, lt_.stop, 0,        \
+                            __VA_ARGS__);                                                      \
+    } else {                                                                                   \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                     \
+    }                                                                                          \
+  } while (0)
 
 // XCDs the dispatcher spreads a launch's blocks over (block i to XCD i mod 8);
 // each has its own L2

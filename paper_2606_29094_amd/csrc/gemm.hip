@@ -146,15 +146,15 @@ static hipError_t launch_rs(const T* A, int lda, const T* B, int ldb, int M, int
   const int kps = splits == 1 ? ceil_div(K, BK) * BK : K / splits;
   if (M <= 32) {
     dim3 g(ceil_div(N, 128), ceil_div(M, 32), splits);
-    hipLaunchKernelGGL((gemm_nt_kernel<T, 32, 128, 1, 4, Epi>), g, dim3(256), 0, st,
+    DLM_LAUNCH((gemm_nt_kernel<T, 32, 128, 1, 4, Epi>), g, dim3(256), 0, st,
                        A, lda, B, ldb, M, N, K, kps, epi);
   } else if (M <= 64) {
     dim3 g(ceil_div(N, 128), ceil_div(M, 64), splits);
-    hipLaunchKernelGGL((gemm_nt_kernel<T, 64, 128, 2, 2, Epi>), g, dim3(256), 0, st,
+    DLM_LAUNCH((gemm_nt_kernel<T, 64, 128, 2, 2, Epi>), g, dim3(256), 0, st,
                        A, lda, B, ldb, M, N, K, kps, epi);
   } else {
     dim3 g(ceil_div(N, 128), ceil_div(M, 128), splits);
-    hipLaunchKernelGGL((gemm_nt_kernel<T, 128, 128, 2, 2, Epi>), g, dim3(256), 0, st,
+    DLM_LAUNCH((gemm_nt_kernel<T, 128, 128, 2, 2, Epi>), g, dim3(256), 0, st,
                        A, lda, B, ldb, M, N, K, kps, epi);
   }
   return hipGetLastError();

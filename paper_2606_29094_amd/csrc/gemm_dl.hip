@@ -253,7 +253,7 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
 #define X(id, BM_, BN_, WM_, WN_, S_, RB_)                                                 \
   case id: {                                                                             \
     dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                  \
-    hipLaunchKernelGGL((gemm_dl_kernel<BM_, BN_, WM_, WN_, S_, RB_, Epi>), g,             \
+    DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, S_, RB_, Epi>), g,             \
                        dim3(WM_ * WN_ * 64),                                             \
                        0, st, A, lda, B, ldb, M, N, K, kps, group_m, epi);                        \
     return hipGetLastError();                                                            \

@@ -32,7 +32,7 @@ template <typename T>
 hipError_t embed_rows(const StepPlan& p, const T* E, int d, int vocab, int mask_id,
                       const int32_t* tokens, const uint8_t* mask, float* h, hipStream_t st) {
   if (p.n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_kernel<T>, dim3(p.n_rows), dim3(256), 0, st, p, E, d, vocab, mask_id,
+  DLM_LAUNCH(embed_kernel<T>, dim3(p.n_rows), dim3(256), 0, st, p, E, d, vocab, mask_id,
                      tokens, mask, h);
   return hipGetLastError();
 }
@@ -156,7 +156,7 @@ template <typename T>
 hipError_t add_rmsnorm_rows(float* h, const float* part, int splits, long stride, const float* g,
                             int n, int d, float eps, T* out, hipStream_t st) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, h, part, splits, stride, g, d,
+  DLM_LAUNCH(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, h, part, splits, stride, g, d,
                      eps, out, (const int*)nullptr, (const int*)nullptr);
   return hipGetLastError();
 }
@@ -165,7 +165,7 @@ template <typename T>
 hipError_t rmsnorm_rows(const float* h, const float* g, int n, int d, float eps, T* out,
                         hipStream_t st) {
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, const_cast<float*>(h),
+  DLM_LAUNCH(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, const_cast<float*>(h),
                      (const float*)nullptr, 0, 0L, g, d, eps, out, (const int*)nullptr,
                      (const int*)nullptr);
   return hipGetLastError();
@@ -176,7 +176,7 @@ hipError_t final_norm_gather(const float* h, const float* g, const int* lm_rows,
                              const int* lm_count, int m_max, int d, float eps, T* u,
                              hipStream_t st) {
   if (m_max == 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(m_max), dim3(256), 0, st, const_cast<float*>(h),
+  DLM_LAUNCH(rmsnorm_kernel<T>, dim3(m_max), dim3(256), 0, st, const_cast<float*>(h),
                      (const float*)nullptr, 0, 0L, g, d, eps, u, lm_rows, lm_count);
   return hipGetLastError();
 }
@@ -197,7 +197,7 @@ __global__ void rope_table_kernel(StepPlan p, int half, double log_theta, float2
 
 hipError_t rope_table(const StepPlan& p, int head_dim, float theta, float2* cs, hipStream_t st) {
   if (p.n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_table_kernel, dim3(p.n_rows), dim3(64), 0, st, p, head_dim / 2,
+  DLM_LAUNCH(rope_table_kernel, dim3(p.n_rows), dim3(64), 0, st, p, head_dim / 2,
                      log((double)theta), cs);
   return hipGetLastError();
 }
@@ -336,7 +336,7 @@ hipError_t qkv_rope_scatter(const StepPlan& p, const float* qkv, int splits, lon
   dim3 g(p.n_tiles, hq + hkv);
   const bool many = (long)p.n_tiles * (hq + hkv) >= 1024;   // four or more blocks per CU
 #define ROPE_LAUNCH(DH_, NTH_)                                                                   \
-  hipLaunchKernelGGL((qkv_rope_scatter_kernel<T, DH_, NTH_>), g, dim3(NTH_), 0, st, p, qkv,     \
+  DLM_LAUNCH((qkv_rope_scatter_kernel<T, DH_, NTH_>), g, dim3(NTH_), 0, st, p, qkv,     \
                      splits, split_stride, cs, hq, hkv, q_out, kcache, vcache, s_max)
   if (dh == 128) {
     if (many) ROPE_LAUNCH(128, 256); else ROPE_LAUNCH(128, 1024);
@@ -397,7 +397,7 @@ __global__ __launch_bounds__(1024) void lm_select_kernel(StepPlan p, const uint8
 
 hipError_t lm_select_rows(const StepPlan& p, const uint8_t* mask, int all_rows, int* lm_rows,
                           int* lm_count, int* req_lm_off, int* req_lm_cnt, hipStream_t st) {
-  hipLaunchKernelGGL(lm_select_kernel, dim3(1), dim3(1024), 0, st, p, mask, all_rows, lm_rows,
+  DLM_LAUNCH(lm_select_kernel, dim3(1), dim3(1024), 0, st, p, mask, all_rows, lm_rows,
                      lm_count, req_lm_off, req_lm_cnt);
   return hipGetLastError();
 }
@@ -446,7 +446,7 @@ __global__ void lm_combine_kernel(const float* __restrict__ pm, const float* __r
 hipError_t lm_combine(const float* pm, const float* ps, const int* pi, int tiles, int ld,
                       const int* lm_count, int m_max, float* conf, int* tok, hipStream_t st) {
   if (m_max == 0) return hipSuccess;
-  hipLaunchKernelGGL(lm_combine_kernel, dim3(m_max), dim3(64), 0, st, pm, ps, pi, tiles, ld,
+  DLM_LAUNCH(lm_combine_kernel, dim3(m_max), dim3(64), 0, st, pm, ps, pi, tiles, ld,
                      lm_count, conf, tok);
   return hipGetLastError();
 }
@@ -593,7 +593,7 @@ hipError_t unmask_select(const StepPlan& p, const float* conf, const int* tok,
                          int32_t* n_unmasked, int32_t* out_pos, int32_t* out_tok,
                          float* out_conf, float* blk_conf, int32_t* blk_tok, float* tok_conf,
                          float* stats, hipStream_t st) {
-  hipLaunchKernelGGL(unmask_kernel, dim3(p.n_req), dim3(kUnmaskThreads), 0, st, p, conf, tok,
+  DLM_LAUNCH(unmask_kernel, dim3(p.n_req), dim3(kUnmaskThreads), 0, st, p, conf, tok,
                      req_lm_off, tokens, mask, n_unmasked, out_pos, out_tok, out_conf, blk_conf,
                      blk_tok, tok_conf, stats);
   return hipGetLastError();

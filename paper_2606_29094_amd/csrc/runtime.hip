@@ -16,6 +16,10 @@
 
 using namespace dlm;
 
+namespace dlm {
+thread_local LaunchTiming g_launch_timing;
+}
+
 namespace {
 
 thread_local std::string g_err;
@@ -43,21 +47,30 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Enqueue `expr` (a launch returning hipError_t) bracketed by timing events
 // when the model's profiler is on.
+// Enqueue one kernel class; when the profiler times this launch, its kernel
+// carries a pair of events in its own dispatch (DLM_LAUNCH), so the measured
+// time is the kernel's and the stream gets no extra commands. (A class that
+// enqueues no kernel this time returns the events unused.)
 #define LAUNCH(model, stream, name, expr)                                           \
   do {                                                                            \
     Profiler& pf_ = (model)->prof;                                                \
     hipEvent_t a_ = nullptr, b_ = nullptr;                                        \
-    const bool t_ = pf_.wants(name);                                              \
-    if (t_) {                                                                     \
+    if (pf_.wants(name)) {                                                        \
       a_ = pf_.take();                                                            \
       b_ = pf_.take();                                                            \
-      if (a_) (void)hipEventRecord(a_, stream);                                   \
+      if (a_ && b_) g_launch_timing = LaunchTiming{a_, b_};                       \
     }                                                                             \
-    HIPCHECK(expr);                                                               \
-    if (t_ && a_ && b_) {                                                         \
-      (void)hipEventRecord(b_, stream);                                           \
+    const hipError_t le_ = (expr);                                                \
+    const bool used_ = a_ && b_ && !g_launch_timing.start;                        \
+    g_launch_timing = LaunchTiming{};                                             \
+    if (used_) {                                                                  \
       pf_.pending.push_back({pf_.kind_of(name), a_, b_});                         \
+    } else {                                                                      \
+      if (a_) pf_.pool.push_back(a_);                                             \
+      if (b_) pf_.pool.push_back(b_);                                             \
     }                                                                             \
+    if (le_ != hipSuccess)                                                        \
+      return fail(DLM_EHIP, "%s failed: %s", #expr, hipGetErrorString(le_));      \
   } while (0)
 
 // Per-kernel-class event timing (dlm_profile_*).
