@@ -205,11 +205,12 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
 
 /* Kernel timing. While enabled, every kernel the library enqueues for this
  * model (or, when only_class is not NULL, every kernel of that class; see also
- * dlm_profile_sample) is bracketed by a pair of HIP events on the launch
- * stream. dlm_profile_read waits for those events, adds their elapsed times
+ * dlm_profile_sample) is timed by a pair of HIP events carried in the kernel's
+ * own dispatch (start and end of the kernel; no extra commands on the
+ * stream). dlm_profile_read waits for those events, adds their elapsed times
  * per kernel class into out[0 .. *n_out) (at most cap entries, in first-seen
- * order) and clears them. Each timed launch costs two event records on the
- * host and a few microseconds of GPU idle time around the launch. */
+ * order) and clears them. A class that enqueues several kernels has its first
+ * one timed. The profiler state is per model and not thread-safe. */
 typedef struct dlm_profile_entry {
   char name[32];          /* kernel class, e.g. "gemm_gate_up_swiglu"                  */
   int32_t calls;          /* launches timed                                             */
