@@ -12,7 +12,7 @@ import torch
 import oracle
 import synth
 from helpers import CONF_TOL, LOGIT_TOL, device_model, host_weights, logit_err, top2_gap
-from paper_2606_29094_amd import engine
+from paper_2606_29094_amd import dlm, engine
 
 pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "tiny_fp32.json")
@@ -164,3 +164,28 @@ def test_cache_modes_teacher_forced(tiny, mode):
         kinds.append(res.refresh)
         _compare_step(res, {k: v[0] for k, v in out.items()}, blk_start, thr)
     assert kinds[0] and not all(kinds)
+
+
+def test_profiler_sampling_counts(tiny):
+    """Kernel timing with sampling: every launch of the selected class is
+    counted, one in `every` is timed (events carried by the kernel's dispatch),
+    and the timed durations are positive."""
+    cfg, model, W, g = tiny
+    prompt, G, thr = synth.request(synth.C1, 0)
+    eng = _engine(model, "none")
+    r = engine.Request(prompt, G, 32, thr)
+    eng.admit(r, cfg.mask_id)
+    dlm.profile_sample(model.handle, 3)
+    dlm.profile_enable(model.handle, True, "gemm_qkv")
+    n_steps = 0
+    while n_steps < 4 and not r.done:
+        eng.step([r])
+        n_steps += 1
+    dlm.profile_enable(model.handle, False)
+    prof = dlm.profile_read(model.handle)
+    dlm.profile_sample(model.handle, 1)
+    launches = n_steps * cfg.n_layers
+    calls, ms, seen = prof["gemm_qkv"]
+    assert seen == launches and calls == (launches + 2) // 3
+    assert ms > 0 and set(prof) == {"gemm_qkv"}
+    assert dlm.profile_read(model.handle) == {}
