@@ -177,8 +177,10 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // model shapes at M = 256 .. 8192, every split, weights streamed from HBM),
 // interpolated linearly in k-tiles (proportionally outside the measured range);
 // a last, partly filled round of a multi-block configuration costs
-// max(0.7, fill) of a full one. When K is split, the fp32 slices add their HBM
-// traffic (written by the GEMM, read back by the consumer). The cheapest
+// max(0.7, fill) of a full one. When K is split, the extra fp32 slices add
+// the consumer's reads of them (their writes are inside the measured round
+// times; charging both picked worse plans, e.g. 62 vs 52 us for the 512-row
+// MHA QKV projection). The cheapest
 // (configuration, split) wins. 128x192 with two blocks per CU (cfg 22) runs
 // without K splits only (its table holds unsplit launches); the small tiles
 // only for few rows.
@@ -251,7 +253,7 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
       double rounds = (double)full;
       if (fill > 0) rounds += c.occ > 1 ? std::max(0.7, fill) : 1.0;
       double t = rounds * round_us(c, (double)(K / s) / 64.0);
-      if (s > 1) t += (double)M * N * 4.0 * 2.0 * (s - 1) / 5.0e12 * 1e6;
+      if (s > 1) t += (double)M * N * 4.0 * (s - 1) / 5.0e12 * 1e6;
       if (t < best_t * 0.999) {
         best_t = t;
         best = GemmPlan{c.cfg, s, 0};

@@ -16,13 +16,13 @@
 
 namespace dlm {
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int SB, int RB, class Epi>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, class Epi>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int k_per_split, int group_m, Epi epi) {
   static_assert(RB == 64 || RB == 128, "k-tile row bytes");
-  static_assert(SB >= 2 && SB <= 4, "B stages");
-  constexpr int SA = 2;                   // A (activation) stages
+  static_assert(SA >= 2 && SA <= 3 && SB >= SA && SB <= 4, "A and B stages");
+  constexpr int DA = SA - 1, DB = SB - 1;  // prefetch distances (k-tiles ahead)
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   constexpr int FM = TM / 16, FN = TN / 16;
@@ -33,7 +33,10 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   constexpr int STAGE_A = BM * RB, STAGE_B = BN * RB;
   constexpr int PERW_A = BM / RPI / NW, PERW_B = BN / RPI / NW;
   static_assert(PERW_A * NW * RPI == BM && PERW_B * NW * RPI == BN, "rows per wave");
-  static_assert(PERW_B < 64, "vmcnt range");
+  // loads of a wave that may stay in flight at the top of an iteration: those
+  // issued after A(kt) in the steady issue order (see the pipeline below)
+  constexpr int INFLIGHT = DB > DA ? DA * PERW_B + (DA - 1) * PERW_A : (DA - 1) * (PERW_A + PERW_B);
+  static_assert(INFLIGHT < 64, "vmcnt range");
   __shared__ __attribute__((aligned(1024))) char smem[SA * STAGE_A + SB * STAGE_B];
   char* const smem_b = smem + SA * STAGE_A;
 
@@ -191,51 +194,53 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     }
   };
 
-  // Pipeline: weights (B) run SB - 1 k-tiles ahead through an SB-stage ring,
-  // activations (A, mostly cache-resident) one k-tile ahead through two
-  // stages. Issue order: B(0) .. B(SB-2), A(0); then iteration kt issues
-  // A(kt+1) followed by B(kt+SB-1). At the top of iteration kt the loads that
-  // may still be in flight are exactly those issued after A(kt): B(kt+SB-2)
-  // when SB >= 3 (vmcnt counts this wave's loads in issue order).
+  // Pipeline: activations (A, mostly cache-resident) run DA = SA - 1 k-tiles
+  // ahead through an SA-stage ring, weights (B, streamed from HBM) DB = SB - 1
+  // ahead through an SB-stage ring. Iteration j issues A(j + DA) then
+  // B(j + DB); the prologue issues the same sequence for j = -DB .. -1. vmcnt
+  // counts a wave's loads in issue order, so at the top of iteration kt the
+  // loads that may stay in flight while A(kt) and B(kt) must have landed are
+  // exactly those issued after A(kt): INFLIGHT of them (everything issued
+  // before A(kt) has landed by then, which is why a deeper B ring needs A
+  // issued further ahead as well). Near the end, where fewer loads were
+  // issued, the wait drains everything.
 #pragma unroll
-  for (int t = 0; t < SB - 1; ++t)
-    if (t < nkt) issue_b(t, ktile(t));
-  if (nkt > 0) issue_a(0, ktile(0));
+  for (int j = -DB; j < 0; ++j) {
+    if (j + DA >= 0 && j + DA < nkt) issue_a((j + DA) % SA, ktile(j + DA));
+    if (j + DB < nkt) issue_b((j + DB) % SB, ktile(j + DB));
+  }
 
   for (int kt = 0; kt < nkt; ++kt) {
-    if constexpr (SB >= 3) {
-      if (kt > 0 && kt + SB - 2 < nkt) wait_vmcnt<PERW_B>(); else wait_vmcnt<0>();
-    } else {
-      wait_vmcnt<0>();
-    }
+    if (INFLIGHT > 0 && kt + DB - 1 < nkt) wait_vmcnt<INFLIGHT>(); else wait_vmcnt<0>();
     // Every wave has its own loads of tile kt in LDS and has finished reading
     // the stages about to be refilled (read at kt - 1). A bare s_barrier:
     // __syncthreads() would add a fence that drains every load in flight.
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if (kt + 1 < nkt) issue_a((kt + 1) & 1, ktile(kt + 1));
-    if (kt + SB - 1 < nkt) issue_b((kt + SB - 1) % SB, ktile(kt + SB - 1));
-    compute(kt & 1, kt % SB);
+    if (kt + DA < nkt) issue_a((kt + DA) % SA, ktile(kt + DA));
+    if (kt + DB < nkt) issue_b((kt + DB) % SB, ktile(kt + DB));
+    compute(kt % SA, kt % SB);
   }
   __syncthreads();
   epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
 }
 
-// Tile configurations (BM, BN, waves M x N, weight stages, k-tile row bytes).
-#define DL_CONFIGS(X)            \
-  X(1, 128, 128, 2, 2, 2, 128)   \
-  X(6, 256, 256, 2, 4, 2, 128)   \
-  X(10, 64, 128, 2, 2, 2, 128)   \
-  X(11, 64, 128, 2, 2, 3, 128)   \
-  X(21, 256, 192, 4, 2, 2, 128)  \
-  X(22, 128, 192, 2, 2, 2, 128)  \
-  X(29, 256, 128, 4, 2, 3, 128)  \
-  X(42, 128, 192, 2, 2, 3, 128)  \
-  X(43, 256, 128, 4, 2, 4, 128)
+// Tile configurations (BM, BN, waves M x N, activation stages, weight stages,
+// k-tile row bytes).
+#define DL_CONFIGS(X)               \
+  X(1, 128, 128, 2, 2, 2, 2, 128)   \
+  X(6, 256, 256, 2, 4, 2, 2, 128)   \
+  X(10, 64, 128, 2, 2, 2, 2, 128)   \
+  X(11, 64, 128, 2, 2, 2, 3, 128)   \
+  X(21, 256, 192, 4, 2, 2, 2, 128)  \
+  X(22, 128, 192, 2, 2, 2, 2, 128)  \
+  X(29, 256, 128, 4, 2, 2, 3, 128)  \
+  X(42, 128, 192, 2, 2, 2, 3, 128)  \
+  X(43, 256, 128, 4, 2, 2, 4, 128)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, S_, RB_) \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_) \
   case id: *bm = BM_; *bn = BN_; *threads = WM_ * WN_ * 64; return 1;
     DL_CONFIGS(X)
 #undef X
@@ -250,10 +255,10 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
   if (K % 64 != 0 || splits < 1 || (K / 64) % splits != 0) return hipErrorInvalidValue;
   const int kps = K / splits;
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, S_, RB_)                                                 \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_)                                            \
   case id: {                                                                             \
     dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                  \
-    DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, S_, RB_, Epi>), g,             \
+    DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, Epi>), g,        \
                        dim3(WM_ * WN_ * 64),                                             \
                        0, st, A, lda, B, ldb, M, N, K, kps, group_m, epi);                        \
     return hipGetLastError();                                                            \
