@@ -100,7 +100,9 @@ typedef struct dlm_weights {
 } dlm_weights;
 
 /* One request of a batched step (host struct). Positions are 0-based within the
- * request; position j of request r lives at tokens[tok_offset + j]. */
+ * request; position j of request r lives at tokens[tok_offset + j]. The ranges
+ * [tok_offset, tok_offset + seq_len) of the requests of one batch must not
+ * overlap (DLM_EINVAL otherwise). */
 typedef struct dlm_req {
   int32_t slot;           /* cache slot, unique within a batch                          */
   int32_t seq_len;        /* prompt + generation length                                  */

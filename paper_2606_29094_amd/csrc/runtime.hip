@@ -4,10 +4,13 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
+#include <cstdint>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/dlm.h"
@@ -45,9 +48,8 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace
 
-// Enqueue `expr` (a launch returning hipError_t) bracketed by timing events
-// when the model's profiler is on.
-// Enqueue one kernel class; when the profiler times this launch, its kernel
+// Enqueue one kernel class (`expr`, a launch returning hipError_t); when the
+// model's profiler times this launch, its kernel
 // carries a pair of events in its own dispatch (DLM_LAUNCH), so the measured
 // time is the kernel's and the stream gets no extra commands. (A class that
 // enqueues no kernel this time returns the events unused.)
@@ -288,6 +290,18 @@ dlm_status make_plan(const dlm_model* m, const dlm_cache* c, const dlm_batch* b,
     tile += ceil_div(rp.nrows, kQTile);
     blk += q.block_len;
   }
+  // the requests' packed token ranges must be disjoint (each step updates its
+  // request's tokens and mask in place)
+  std::vector<std::pair<long, long>> ranges(b->n_req);
+  for (int r = 0; r < b->n_req; ++r)
+    ranges[r] = {(long)b->reqs[r].tok_offset, (long)b->reqs[r].tok_offset + b->reqs[r].seq_len};
+  std::sort(ranges.begin(), ranges.end());
+  for (int r = 1; r < b->n_req; ++r)
+    if (ranges[r].first < ranges[r - 1].second)
+      return fail(DLM_EINVAL, "token ranges [%ld, %ld) and [%ld, %ld) overlap", ranges[r - 1].first,
+                  ranges[r - 1].second, ranges[r].first, ranges[r].second);
+  if (ranges.back().second > INT32_MAX)
+    return fail(DLM_EINVAL, "token range end %ld exceeds the int32 index range", ranges.back().second);
   p->n_rows = row;
   p->n_tiles = tile;
   p->n_blk = blk;
@@ -493,7 +507,7 @@ dlm_status dlm_profile_sample(dlm_model* m, int32_t every) {
 
 dlm_status dlm_profile_read(dlm_model* m, dlm_profile_entry* out, int32_t cap, int32_t* n_out) {
   g_err.clear();
-  if (!m || !n_out || (cap > 0 && !out)) return fail(DLM_EINVAL, "NULL argument");
+  if (!m || !n_out || cap < 0 || (cap > 0 && !out)) return fail(DLM_EINVAL, "NULL argument or cap < 0");
   Profiler& pf = m->prof;
   std::vector<int> calls(pf.names.size(), 0);
   std::vector<double> ms(pf.names.size(), 0.0);
@@ -533,11 +547,11 @@ dlm_status dlm_workspace_bytes(const dlm_model* m, int32_t max_rows, int32_t max
   if (!m || !out_bytes) return fail(DLM_EINVAL, "NULL argument");
   if (max_rows < 1 || max_reqs < 1 || max_reqs > kMaxReq)
     return fail(DLM_EINVAL, "max_rows %d / max_reqs %d out of range", max_rows, max_reqs);
-  // split counts grow as rows shrink: take the largest layout over row counts
+  // the planner's split-K factors (and with them the slice buffers) depend on
+  // the row count and are not monotonic in it: take the largest layout over
+  // every row count up to max_rows
   size_t best = 0;
-  for (int n = 1; n <= max_rows; n = n < 64 ? n + 1 : n + 16)
-    best = std::max(best, layout(m, n, max_reqs).total);
-  best = std::max(best, layout(m, max_rows, max_reqs).total);
+  for (int n = 1; n <= max_rows; ++n) best = std::max(best, layout(m, n, max_reqs).total);
   *out_bytes = best;
   return DLM_OK;
 }

@@ -179,6 +179,41 @@ def test_duplicate_slot_and_workspace_checks():
     assert "aligned" in dlm.last_error()
 
 
+def test_token_ranges_must_not_overlap():
+    _lib_or_skip()
+    m = _load()
+    c = _cache(m)
+    with pytest.raises(dlm.DlmError) as e:
+        _step(m, c, [_req(slot=0, flags=1), _req(slot=1, flags=1, off=50)])
+    assert e.value.status == dlm.DLM_EINVAL and "overlap" in dlm.last_error()
+    # disjoint ranges pass the plan checks (and stop at the too-small workspace)
+    with pytest.raises(dlm.DlmError) as e:
+        _step(m, c, [_req(slot=0, flags=1), _req(slot=1, flags=1, off=96)], ws=_Buf(0x800000, 1024))
+    assert e.value.status == dlm.DLM_ESIZE, dlm.last_error()
+    dlm.model_destroy(m)
+
+
+@pytest.mark.parametrize("dims", [
+    dict(),
+    dict(d_model=4096, n_q_heads=32, n_kv_heads=32, head_dim=128, d_ffn=12288, vocab=126464,
+         mask_id=126336, dtype=dlm.DLM_BF16),
+    dict(d_model=3584, n_q_heads=28, n_kv_heads=4, head_dim=128, d_ffn=18944, vocab=152064,
+         mask_id=151666, dtype=dlm.DLM_BF16),
+])
+def test_workspace_bytes_is_monotonic_in_rows(dims):
+    # the split-K slice buffers depend on the planner's choice for each row
+    # count; the size query must cover every row count up to max_rows, so it
+    # can never shrink as max_rows grows
+    _lib_or_skip()
+    m = _load(_cfg(**dims))
+    prev = 0
+    for n in range(1, 1100):
+        w = dlm.workspace_bytes(m, n, 8)
+        assert w >= prev, n
+        prev = w
+    dlm.model_destroy(m)
+
+
 def test_engine_request_block_bookkeeping():
     from paper_2606_29094_amd.engine import Request
     r = Request(np.arange(10), 70, 32, 0.9)
