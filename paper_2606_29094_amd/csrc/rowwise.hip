@@ -63,7 +63,11 @@ __device__ __forceinline__ void store4(bf16* o, float a, float b, float c, float
   *reinterpret_cast<bf16x4*>(o) = v;
 }
 
-template <typename T>
+// S > 0: exactly S split-K slices, all of a row's slice loads issued before
+// the first add (the row's partials are in flight at once instead of one
+// slice per memory round trip); S == 0: `splits` slices, one at a time.
+// Either way the sum is h + slice 0 + slice 1 + ... in that order.
+template <typename T, int S>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ h,
                                                       const float* __restrict__ part, int splits,
                                                       long stride, const float* __restrict__ g,
@@ -87,19 +91,42 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ h,
       if (j < d) v[c] = *reinterpret_cast<const float4*>(x + j);
     }
     if (part) {
-      for (int sl = 0; sl < splits; ++sl) {
-        const float* ps = part + sl * stride + (long)src_row * d;
-        float4 pv[4];
+      if constexpr (S > 0) {
+        float4 pv[S][4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int j = threadIdx.x * 4 + c * 1024;
-          if (j < d) pv[c] = *reinterpret_cast<const float4*>(ps + j);
+        for (int sl = 0; sl < S; ++sl) {
+          const float* ps = part + sl * stride + (long)src_row * d;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int j = threadIdx.x * 4 + c * 1024;
+            if (j < d) pv[sl][c] = *reinterpret_cast<const float4*>(ps + j);
+          }
         }
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int j = threadIdx.x * 4 + c * 1024;
-          if (j < d) {
-            v[c].x += pv[c].x; v[c].y += pv[c].y; v[c].z += pv[c].z; v[c].w += pv[c].w;
+        for (int sl = 0; sl < S; ++sl)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int j = threadIdx.x * 4 + c * 1024;
+            if (j < d) {
+              v[c].x += pv[sl][c].x; v[c].y += pv[sl][c].y;
+              v[c].z += pv[sl][c].z; v[c].w += pv[sl][c].w;
+            }
+          }
+      } else {
+        for (int sl = 0; sl < splits; ++sl) {
+          const float* ps = part + sl * stride + (long)src_row * d;
+          float4 pv[4];
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int j = threadIdx.x * 4 + c * 1024;
+            if (j < d) pv[c] = *reinterpret_cast<const float4*>(ps + j);
+          }
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int j = threadIdx.x * 4 + c * 1024;
+            if (j < d) {
+              v[c].x += pv[c].x; v[c].y += pv[c].y; v[c].z += pv[c].z; v[c].w += pv[c].w;
+            }
           }
         }
       }
@@ -156,8 +183,17 @@ template <typename T>
 hipError_t add_rmsnorm_rows(float* h, const float* part, int splits, long stride, const float* g,
                             int n, int d, float eps, T* out, hipStream_t st) {
   if (n == 0) return hipSuccess;
-  DLM_LAUNCH(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, h, part, splits, stride, g, d,
-                     eps, out, (const int*)nullptr, (const int*)nullptr);
+#define ADD_NORM(S_)                                                                         \
+  DLM_LAUNCH((rmsnorm_kernel<T, S_>), dim3(n), dim3(256), 0, st, h, part, splits, stride, g, \
+             d, eps, out, (const int*)nullptr, (const int*)nullptr)
+  switch (d <= 4096 ? splits : 0) {
+    case 1: ADD_NORM(1); break;
+    case 2: ADD_NORM(2); break;
+    case 4: ADD_NORM(4); break;
+    case 8: ADD_NORM(8); break;
+    default: ADD_NORM(0); break;
+  }
+#undef ADD_NORM
   return hipGetLastError();
 }
 
@@ -165,7 +201,7 @@ template <typename T>
 hipError_t rmsnorm_rows(const float* h, const float* g, int n, int d, float eps, T* out,
                         hipStream_t st) {
   if (n == 0) return hipSuccess;
-  DLM_LAUNCH(rmsnorm_kernel<T>, dim3(n), dim3(256), 0, st, const_cast<float*>(h),
+  DLM_LAUNCH((rmsnorm_kernel<T, 0>), dim3(n), dim3(256), 0, st, const_cast<float*>(h),
                      (const float*)nullptr, 0, 0L, g, d, eps, out, (const int*)nullptr,
                      (const int*)nullptr);
   return hipGetLastError();
@@ -176,7 +212,7 @@ hipError_t final_norm_gather(const float* h, const float* g, const int* lm_rows,
                              const int* lm_count, int m_max, int d, float eps, T* u,
                              hipStream_t st) {
   if (m_max == 0) return hipSuccess;
-  DLM_LAUNCH(rmsnorm_kernel<T>, dim3(m_max), dim3(256), 0, st, const_cast<float*>(h),
+  DLM_LAUNCH((rmsnorm_kernel<T, 0>), dim3(m_max), dim3(256), 0, st, const_cast<float*>(h),
                      (const float*)nullptr, 0, 0L, g, d, eps, u, lm_rows, lm_count);
   return hipGetLastError();
 }
