@@ -71,6 +71,26 @@ def test_mha_cache_steps_ragged_batch(mha, mode):
     assert any(st["kinds"]) and not all(st["kinds"])
 
 
+def test_mha_cache_steps_long_keys(mha):
+    """Recompute then cache steps of three requests with longer, ragged key
+    ranges (600, 200 and 520 positions; 32-row cache steps attend over all of
+    them)."""
+    cfg, t, W = mha
+    specs = [(504, 96), (136, 64), (424, 96)]
+    prompts = [synth.tokens(700 + i, p, cfg.vocab) for i, (p, _) in enumerate(specs)]
+    gammas = [0.9, 0.8, 0.95]
+    oreqs = [oracle.Request.new(p, g, 32, gm, cfg.mask_id)
+             for p, (_, g), gm in zip(prompts, specs, gammas)]
+    inv_tau = calibrated_inv_tau(cfg, W, oreqs, "dual")
+    eng = engine.Engine(_model(cfg, t, inv_tau), 3, 640, "dual")
+    reqs = [engine.Request(p, g, 32, gm) for p, (_, g), gm in zip(prompts, specs, gammas)]
+    for r in reqs:
+        eng.admit(r, cfg.mask_id)
+    st = run_teacher_forced(cfg, W, eng, reqs, oreqs, "dual", inv_tau, 3)
+    print("long keys:", st)
+    assert any(st["kinds"]) and not all(st["kinds"])
+
+
 def test_gqa_dual_refresh_then_cache(gqa):
     """GQA (28 query / 4 kv heads), blocks of 64, dual cache."""
     cfg, t, W = gqa
