@@ -155,11 +155,18 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
       }
     }
   };
+  // K rows are stored in the permuted key order of the shared-tile kernel:
+  // inside each group of 32 keys, key 8 g + 4 h + i goes to row 16 h + 4 g + i
+  // (h < 2, g < 4, i < 4), so the S^T values lane group g owns are the keys
+  // 8 g .. 8 g + 7 of each 32-key group and V^T is read as one 16-byte chunk
+  // per lane
   auto store_tile = [&]() {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int c = tid + i * NT;
-      *reinterpret_cast<u32x4*>(ks + (c / (DH / 8)) * KS + (c % (DH / 8)) * 8) = kreg[i];
+      const int k = c / (DH / 8);
+      const int row = (k & ~31) | (((k >> 2) & 1) << 4) | (((k >> 3) & 3) << 2) | (k & 3);
+      *reinterpret_cast<u32x4*>(ks + row * KS + (c % (DH / 8)) * 8) = kreg[i];
     }
 #pragma unroll
     for (int i = 0; i < VCH; ++i) {
@@ -177,7 +184,8 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
     if (t + 1 < ntiles) load_tile((t + 1) * SK);
     const bf16* ksg = ks + kg * 64 * KS;
 
-    // S^T blocks: sblk[kb][i] = raw score(key = key0 + 16*kb + 4*g + i, query = lane&15)
+    // S^T blocks: sblk[kb][i] = raw score(key = key0 + 32 (kb / 2) + 8 g + 4 (kb % 2) + i,
+    // query = lane&15)
     f32x4 sblk[4];
 #pragma unroll
     for (int kbk = 0; kbk < 4; ++kbk) {
@@ -194,7 +202,7 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
       for (int kbk = 0; kbk < 4; ++kbk)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (key0 + kbk * 16 + 4 * g + i >= L) sblk[kbk][i] = -INFINITY;
+          if (key0 + 32 * (kbk >> 1) + 8 * g + 4 * (kbk & 1) + i >= L) sblk[kbk][i] = -INFINITY;
     }
     float mt = -INFINITY;
 #pragma unroll
@@ -226,7 +234,7 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
     l_run += lsum;
 
     // O^T += V^T P^T over two 32-key steps; B operand slot 8g+e <-> key
-    // 32*j + (e < 4 ? 4g + e : 16 + 4g + e - 4)
+    // 32*j + 8g + e (sblk[2j] holds keys 8g..8g+3, sblk[2j+1] keys 8g+4..8g+7)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       bf16x8 ph, pl;
@@ -238,10 +246,8 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const bf16* vrow = vs + (db * 16 + (lane & 15)) * VS + kg * 64 + 32 * j + 4 * g;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+        const bf16* vrow = vs + (db * 16 + (lane & 15)) * VS + kg * 64 + 32 * j + 8 * g;
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vrow));
         o[db] = mfma16_bf16(a, ph, o[db]);
         if constexpr (PLO) o[db] = mfma16_bf16(a, pl, o[db]);
       }
