@@ -21,6 +21,7 @@ region), the whole-step roofline, and the CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -300,6 +301,10 @@ def main():
     ap.add_argument("--slo", type=float, default=10.0, help="latency SLO of --serve (s)")
     ap.add_argument("--fixed-threshold", type=float, default=None,
                     help="--serve with this single threshold instead of the controller's choice")
+    ap.add_argument("--tp-share", type=int, default=1, metavar="N",
+                    help="run one tensor-parallel rank's share of the model on this GPU: "
+                         "1/N of the query/key-value heads, FFN columns and vocabulary at the "
+                         "same rows (the rank's compute only; no collectives)")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-loop and copy ceilings")
     args = ap.parse_args()
@@ -335,6 +340,18 @@ def main():
         inv_tau, tau_src = args.inv_tau, "command line"
     else:
         inv_tau, tau_src = load_inv_tau(cfg.name)
+    tp = args.tp_share
+    if tp > 1:
+        # one rank of tensor parallelism: heads, FFN columns and vocabulary
+        # split N ways (QKV / gate-up column-parallel, O / down row-parallel,
+        # vocabulary-parallel head); prompt tokens are folded into the shard's
+        # vocabulary (the rank's work does not depend on their values)
+        if cfg.n_q_heads % tp or cfg.n_kv_heads % tp or cfg.d_ffn % (16 * tp) or cfg.vocab % tp:
+            raise SystemExit(f"--tp-share {tp} does not divide the {cfg.name} shapes")
+        cfg = dataclasses.replace(cfg, name=f"{cfg.name}-tp{tp}-rank", n_q_heads=cfg.n_q_heads // tp,
+                                  n_kv_heads=cfg.n_kv_heads // tp, d_ffn=cfg.d_ffn // tp,
+                                  vocab=cfg.vocab // tp)
+        w = dataclasses.replace(w, name=f"{w.name}-tp{tp}-rank", model=cfg)
     if args.serve is not None:
         serve_main(args, w, cfg, inv_tau)
         return
@@ -358,6 +375,8 @@ def main():
     def make(slot):
         rid = next_id[slot]
         prompt, G, thr = synth.request(w, rid)
+        if tp > 1:
+            prompt = prompt % cfg.vocab
         if hetero:
             next_id[slot] += B
         if args.threshold is not None:
@@ -486,7 +505,8 @@ def main():
         F, Bb = stats["cls"][dom]
         F1, B1 = F / launches, Bb / launches           # per launch
         avg_s = tot / calls * 1e-3
-        traffic, traffic_src = measured_traffic(dom) if args.workload == "c2" else (None, None)
+        traffic, traffic_src = (measured_traffic(dom) if args.workload == "c2" and tp == 1
+                                else (None, None))
         if F1 / B1 >= ridge:
             achieved = F1 / avg_s / 1e12
             roof = {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": peak,
@@ -510,6 +530,8 @@ def main():
     cpu = None
     if args.cpu_layers > 0:
         prompt, G, _ = synth.request(w, 0)
+        if tp > 1:
+            prompt = prompt % cfg.vocab
         cpu = cpu_baseline(cfg, tensors, prompt, G, w.block, inv_tau, args.cpu_layers)
         if B > 1 or w.cache_mode != "none":
             cpu["sample"] += ("; one request's no-cache step (the timed GPU steps batch "
@@ -536,7 +558,7 @@ def main():
         "ms_per_step": 1e3 * t_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16" if shape.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "batch": B,
+        "config": {"workload": w.name, "batch": B, "tp_share": tp,
                    "prompt_len": w.prompt_len or list(w.prompt_range),
                    "gen_len": w.gen_len or list(w.gen_choices),
                    "block": w.block, "cache": w.cache_mode,
