@@ -273,7 +273,7 @@ def main():
     ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
     ap.add_argument("--threshold", type=float, default=None,
                     help="override every request's threshold (the GQA sweep)")
-    ap.add_argument("--cpu-layers", type=int, default=16,
+    ap.add_argument("--cpu-layers", type=int, default=24,
                     help="layers of the CPU oracle sample (0 disables the CPU baseline)")
     ap.add_argument("--inv-tau", type=float, default=None,
                     help="override the stored calibrated 1/tau")
