@@ -160,11 +160,18 @@ void dlm_model_destroy(dlm_model* m);
 dlm_status dlm_workspace_bytes(const dlm_model* m, int32_t max_rows, int32_t max_reqs,
                                size_t* out_bytes);
 
-/* Carve n_slots fixed KV slots of max_seq_len positions out of the caller's
- * buffer (post-RoPE keys and values of every layer; the output length of a
- * request is known in advance, so slots are fixed-size). With dev_buf == NULL
- * only *required_bytes is written. Every slot starts invalid: its first step
- * must be a recompute step. */
+/* KV cache (paper: "Support for Approximate Caching"; "Supporting Approximate
+ * KV Caching", where the caches are kept in GPU memory and rebuilt by the
+ * recompute steps; "Implementation"). Carve n_slots fixed KV slots of
+ * max_seq_len positions out of the caller's buffer: the post-RoPE keys and
+ * values of every layer, per layer a key region [slot][kv_head][pos][head_dim]
+ * and a transposed value region [slot][kv_head][head_dim][pos], slots rounded
+ * up to 64 positions. A request's output length is known when it arrives
+ * ("Request Scheduling"), so slots are fixed-size and never paged. With
+ * dev_buf == NULL only *required_bytes is written (out may then be NULL).
+ * The buffer must be 256-byte aligned and hold *required_bytes (DLM_ESIZE
+ * otherwise); it stays the caller's. Every slot starts invalid: its first
+ * step must be a recompute step. */
 dlm_status dlm_kv_cache_alloc(const dlm_model* m, int32_t n_slots, int32_t max_seq_len,
                               void* dev_buf, size_t buf_bytes, size_t* required_bytes,
                               dlm_cache** out);
@@ -172,20 +179,36 @@ void dlm_cache_destroy(dlm_cache* c);
 /* Mark a slot stale (its next step must be a recompute step). */
 dlm_status dlm_cache_invalidate(dlm_cache* c, int32_t slot);
 
-/* One batched denoising step. thresholds: host [n_req], each in [0, 1].
+/* One batched denoising step (paper: "Background and Challenges", Diffusion
+ * Language Models, for the forward, the confidence and the threshold rule;
+ * "SLO-aware Confidence Threshold Adjustment" for per-request thresholds; "Supporting
+ * Approximate KV Caching" for recompute and cache steps). thresholds: host
+ * [n_req], each in [0, 1] (DLM_EINVAL otherwise, or for a NaN).
  * Requests flagged DLM_REQ_REFRESH (all requests when mode is DLM_CACHE_NONE)
  * recompute every position and rewrite their slot; the others recompute the
  * rows their mode names and need a slot refreshed at the same block_start
- * (else DLM_ESTATE). Masked positions of the active block get a prediction;
- * those with confidence > threshold are unmasked (tokens[] and mask[] updated
- * in place); if none passes, the most confident one (lowest position on ties)
- * is unmasked. */
+ * and seq_len (else DLM_ESTATE). Masked positions of the active block get a
+ * prediction, the vocabulary argmax (lowest id on ties) of the logits scaled
+ * by inv_tau, and a confidence, its softmax probability; those with
+ * confidence > threshold are unmasked (tokens[] and mask[] updated in place);
+ * if none passes, the most confident one (lowest position on ties) is
+ * unmasked. Outputs and the token/mask updates are device writes, valid once
+ * the stream is synchronised. The workspace (256-byte aligned,
+ * dlm_workspace_bytes for at least this step's rows and requests) is
+ * scratch, overwritten by the step. */
 dlm_status dlm_denoise_step(dlm_model* m, dlm_cache* c, const dlm_batch* b,
                             const float* thresholds, const dlm_step_out* out,
                             void* workspace, size_t ws_bytes, void* stream);
 
-/* Recompute every position of every request of the batch and rewrite their
- * slots without unmasking anything (prefill, resume, or rebuilding a slot). */
+/* Recompute step without unmasking (paper: "Implementation", the caches are
+ * rebuilt during recompute steps; "Request Scheduling", a request migrates or
+ * resumes only at a recompute step): recompute every position of every
+ * request of the batch with the batch's current tokens and mask and rewrite
+ * their slots, marking each slot current for its block_start and seq_len.
+ * Nothing is unmasked and no step output is written; the thresholds are not
+ * needed. Used for prefill, for resuming a migrated or evicted request, or for
+ * rebuilding a slot. Same validation, workspace and stream rules as
+ * dlm_denoise_step. */
 dlm_status dlm_cache_refresh(dlm_model* m, dlm_cache* c, const dlm_batch* b,
                              void* workspace, size_t ws_bytes, void* stream);
 
@@ -196,6 +219,57 @@ dlm_status dlm_cache_refresh(dlm_model* m, dlm_cache* c, const dlm_batch* b,
 dlm_status dlm_debug_logits(dlm_model* m, dlm_cache* c, const dlm_batch* b,
                             float* logits_out, void* workspace, size_t ws_bytes,
                             void* stream);
+
+/* Test hook: the intermediate values of one layer of a step's forward (the
+ * pre-norm layer of "Background and Challenges", Diffusion Language Models:
+ * norm, QKV projection, rotary positions and the key/value write, full
+ * bidirectional attention over the slot, output projection and residual,
+ * norm, SwiGLU feed-forward and residual), copied device to device out of the
+ * workspace as the step's own kernels produce them, so that every kernel can
+ * be checked on the exact inputs it was given. The forward is the one of
+ * dlm_denoise_step (same rows, plans and cache writes; nothing is unmasked).
+ * N is the number of recomputed rows of the step, packed in request order,
+ * positions ascending (a request's rows are [0, seq_len) on a recompute step,
+ * [block_start, block_start + block_len) on a dual-cache step and
+ * [block_start, seq_len) on a prefix-cache step). Every buffer is a device
+ * pointer and optional (NULL records nothing); "model dtype" buffers hold the
+ * storage type (bf16 or fp32), the others fp32:
+ *   h_in   [N, d_model]       residual stream entering the layer
+ *   a_attn [N, d_model]       attention-norm output (model dtype)
+ *   qkv    [qkv_cap, N, (n_q_heads + 2 n_kv_heads) head_dim] fp32 output of
+ *                             the QKV GEMM as K-split slices: slice s holds the
+ *                             sum over the s-th of qkv_splits equal K ranges;
+ *                             the consumer adds slices 0, 1, ... in order
+ *   q      [N, n_q_heads head_dim]  queries after the rotary embedding (model dtype)
+ *   attn_out [N, n_q_heads head_dim] attention output (model dtype)
+ *   h_mid  [N, d_model]       residual stream after the output projection
+ *   a_ffn  [N, d_model]       feed-forward-norm output (model dtype)
+ *   act    [N, d_ffn]         silu(gate) * up (model dtype)
+ *   h_out  [N, d_model]       residual stream after the down projection
+ *   u      [sum block_len, d_model] final-normed rows of every active-block
+ *                             position (model dtype); needs logits
+ *   logits [sum block_len, vocab] scaled logits, as dlm_debug_logits
+ * The keys and values of the layer are in the cache. qkv_splits (out) is the
+ * number of slices the step's QKV GEMM wrote; DLM_ESIZE (nothing enqueued)
+ * when qkv is given and qkv_cap is smaller. */
+typedef struct dlm_trace {
+  int32_t layer;          /* in [0, n_layers)                                           */
+  int32_t qkv_cap;        /* slices the qkv buffer holds                                 */
+  float* h_in;
+  void* a_attn;
+  float* qkv;
+  void* q;
+  void* attn_out;
+  float* h_mid;
+  void* a_ffn;
+  void* act;
+  float* h_out;
+  void* u;
+  float* logits;
+  int32_t qkv_splits;     /* out */
+} dlm_trace;
+dlm_status dlm_debug_trace(dlm_model* m, dlm_cache* c, const dlm_batch* b, dlm_trace* trace,
+                           void* workspace, size_t ws_bytes, void* stream);
 
 /* The fused LM head alone: for each of m_rows final-normed hidden rows
  * (device, [m_rows, d_model] in the model dtype), conf[i] = max softmax(z_i) and

@@ -323,9 +323,16 @@ dlm_status check_ws(const dlm_model* m, const StepPlan& p, void* ws, size_t ws_b
 
 enum class Tail { Unmask, Logits, None };
 
+// Device-to-device copy of a recorded intermediate (dlm_debug_trace); a NULL
+// destination records nothing.
+#define TRACE_COPY(dst, src, bytes)                                                    \
+  do {                                                                                 \
+    if (dst) HIPCHECK(hipMemcpyAsync((dst), (src), (bytes), hipMemcpyDeviceToDevice, st)); \
+  } while (0)
+
 template <typename T>
 dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPlan& p,
-                       const Layout& L, char* ws, hipStream_t st) {
+                       const Layout& L, char* ws, const dlm_trace* tr, hipStream_t st) {
   const dlm_config& cf = m->cfg;
   const int d = cf.d_model, hq = cf.n_q_heads, hkv = cf.n_kv_heads, dh = cf.head_dim;
   const int qkv_dim = (hq + 2 * hkv) * dh, qd = hq * dh, n = p.n_rows;
@@ -342,15 +349,24 @@ dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const Ste
   LAUNCH(m, st, "embed", embed_rows<T>(p, reinterpret_cast<const T*>(m->embed), d, cf.vocab, cf.mask_id,
                          b->tokens, b->mask, h, st));
   LAUNCH(m, st, "rmsnorm", rmsnorm_rows<T>(h, m->layers[0].attn_norm, n, d, cf.rms_eps, a, st));
+  const size_t es = sizeof(T);
   for (int l = 0; l < cf.n_layers; ++l) {
     const dlm_layer_weights& w = m->layers[l];
     T* kc = reinterpret_cast<T*>(c->k_layer(l));
     T* vc = reinterpret_cast<T*>(c->v_layer(l));
+    const dlm_trace* t = tr && tr->layer == l ? tr : nullptr;
+    if (t) {
+      TRACE_COPY(t->h_in, h, (size_t)n * d * 4);
+      TRACE_COPY(t->a_attn, a, (size_t)n * d * es);
+    }
     LAUNCH(m, st, "gemm_qkv", gemm_store_f32<T>(L.g_qkv, a, d, reinterpret_cast<const T*>(w.w_qkv), d, n,
                                                       qkv_dim, d, qkv, qkv_dim, st));
+    if (t) TRACE_COPY(t->qkv, qkv, (size_t)L.s_qkv * n * qkv_dim * 4);
     LAUNCH(m, st, "rope_kv_write", qkv_rope_scatter<T>(p, qkv, L.s_qkv, (long)n * qkv_dim, cs, hq, hkv, dh, q, kc, vc,
                                  c->s_max, st));
+    if (t) TRACE_COPY(t->q, q, (size_t)n * qd * es);
     LAUNCH(m, st, "attention", attention<T>(p, q, kc, vc, c->s_max, hq, hkv, dh, ao, st));
+    if (t) TRACE_COPY(t->attn_out, ao, (size_t)n * qd * es);
     // O projection; its residual update is fused into the FFN norm when K is split
     if (L.s_o == 1) {
       LAUNCH(m, st, "gemm_o", gemm_add_f32<T>(L.g_o, ao, qd, reinterpret_cast<const T*>(w.w_o), qd, n, d,
@@ -362,8 +378,13 @@ dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const Ste
       LAUNCH(m, st, "residual_rmsnorm", add_rmsnorm_rows<T>(h, part, L.s_o, (long)n * d, w.ffn_norm, n, d,
                                                                 cf.rms_eps, a, st));
     }
+    if (t) {
+      TRACE_COPY(t->h_mid, h, (size_t)n * d * 4);
+      TRACE_COPY(t->a_ffn, a, (size_t)n * d * es);
+    }
     LAUNCH(m, st, "gemm_gate_up_swiglu", gemm_swiglu<T>(L.g_gu, a, d, reinterpret_cast<const T*>(w.w_gate_up), d, n, cf.d_ffn, d, act,
                             cf.d_ffn, st));
+    if (t) TRACE_COPY(t->act, act, (size_t)n * cf.d_ffn * es);
     // down projection; its residual update is fused into the next layer's norm
     const float* next_norm = l + 1 < cf.n_layers ? m->layers[l + 1].attn_norm : nullptr;
     T* next_a = l + 1 < cf.n_layers ? a : nullptr;
@@ -377,6 +398,7 @@ dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const Ste
       LAUNCH(m, st, "residual_rmsnorm", add_rmsnorm_rows<T>(h, part, L.s_down, (long)n * d, next_norm, n, d,
                                                                 cf.rms_eps, next_a, st));
     }
+    if (t) TRACE_COPY(t->h_out, h, (size_t)n * d * 4);
   }
   return DLM_OK;
 }
@@ -384,8 +406,8 @@ dlm_status run_forward(dlm_model* m, dlm_cache* c, const dlm_batch* b, const Ste
 template <typename T>
 dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPlan& p,
                     const Layout& L, char* ws, Tail tail, const dlm_step_out* out,
-                    float* logits, hipStream_t st) {
-  dlm_status s = run_forward<T>(m, c, b, p, L, ws, st);
+                    float* logits, const dlm_trace* tr, hipStream_t st) {
+  dlm_status s = run_forward<T>(m, c, b, p, L, ws, tr, st);
   if (s != DLM_OK || tail == Tail::None) return s;
   const dlm_config& cf = m->cfg;
   const int d = cf.d_model;
@@ -399,6 +421,7 @@ dlm_status run_step(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPl
   LAUNCH(m, st, "lm_select", lm_select_rows(p, b->mask, tail == Tail::Logits ? 1 : 0, lm_rows, lm_count, req_off,
                           req_cnt, st));
   LAUNCH(m, st, "final_norm", final_norm_gather<T>(h, m->final_norm, lm_rows, lm_count, m_max, d, cf.rms_eps, u, st));
+  if (tr && tail == Tail::Logits) TRACE_COPY(tr->u, u, (size_t)m_max * d * sizeof(T));
   if (tail == Tail::Logits) {
     LAUNCH(m, st, "gemm_logits", gemm_scaled_f32<T>(L.g_logits, u, d, reinterpret_cast<const T*>(m->lm_head), d, m_max, cf.vocab,
                                 d, cf.inv_tau, logits, cf.vocab, st));
@@ -432,11 +455,11 @@ void mark_refreshed(dlm_cache* c, const dlm_batch* b, bool force_refresh) {
 
 dlm_status dispatch(dlm_model* m, dlm_cache* c, const dlm_batch* b, const StepPlan& p,
                     const Layout& L, void* ws, Tail tail, const dlm_step_out* out,
-                    float* logits, void* stream) {
+                    float* logits, void* stream, const dlm_trace* tr = nullptr) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   char* w = reinterpret_cast<char*>(ws);
-  if (m->cfg.dtype == DLM_BF16) return run_step<bf16>(m, c, b, p, L, w, tail, out, logits, st);
-  return run_step<float>(m, c, b, p, L, w, tail, out, logits, st);
+  if (m->cfg.dtype == DLM_BF16) return run_step<bf16>(m, c, b, p, L, w, tail, out, logits, tr, st);
+  return run_step<float>(m, c, b, p, L, w, tail, out, logits, tr, st);
 }
 
 dlm_status check_handles(dlm_model* m, dlm_cache* c) {
@@ -650,6 +673,31 @@ dlm_status dlm_debug_logits(dlm_model* m, dlm_cache* c, const dlm_batch* b, floa
   s = check_ws(m, p, workspace, ws_bytes, &L);
   if (s != DLM_OK) return s;
   s = dispatch(m, c, b, p, L, workspace, Tail::Logits, nullptr, logits_out, stream);
+  if (s == DLM_OK) mark_refreshed(c, b, false);
+  return s;
+}
+
+dlm_status dlm_debug_trace(dlm_model* m, dlm_cache* c, const dlm_batch* b, dlm_trace* tr,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  dlm_status s = check_handles(m, c);
+  if (s != DLM_OK) return s;
+  if (!tr) return fail(DLM_EINVAL, "trace is NULL");
+  if (tr->layer < 0 || tr->layer >= m->cfg.n_layers)
+    return fail(DLM_EINVAL, "trace layer %d outside [0, %d)", tr->layer, m->cfg.n_layers);
+  if (tr->u && !tr->logits) return fail(DLM_EINVAL, "trace.u needs trace.logits");
+  StepPlan p;
+  s = make_plan(m, c, b, nullptr, false, &p);
+  if (s != DLM_OK) return s;
+  Layout L;
+  s = check_ws(m, p, workspace, ws_bytes, &L);
+  if (s != DLM_OK) return s;
+  if (tr->qkv && tr->qkv_cap < L.s_qkv)
+    return fail(DLM_ESIZE, "trace.qkv holds %d K-split slices; this step writes %d", tr->qkv_cap,
+                L.s_qkv);
+  tr->qkv_splits = L.s_qkv;
+  s = dispatch(m, c, b, p, L, workspace, tr->logits ? Tail::Logits : Tail::None, nullptr,
+               tr->logits, stream, tr);
   if (s == DLM_OK) mark_refreshed(c, b, false);
   return s;
 }

@@ -24,7 +24,7 @@ MODES = {"none": DLM_CACHE_NONE, "prefix": DLM_CACHE_PREFIX, "dual": DLM_CACHE_D
 
 EXPORTS = ["dlm_load_weights", "dlm_model_destroy", "dlm_workspace_bytes",
            "dlm_kv_cache_alloc", "dlm_cache_destroy", "dlm_cache_invalidate",
-           "dlm_denoise_step", "dlm_cache_refresh", "dlm_debug_logits",
+           "dlm_denoise_step", "dlm_cache_refresh", "dlm_debug_logits", "dlm_debug_trace",
            "dlm_head_confidence", "dlm_profile_enable", "dlm_profile_read",
            "dlm_profile_sample", "dlm_ceiling_mfma", "dlm_ceiling_copy", "dlm_last_error"]
 
@@ -63,6 +63,18 @@ class DlmStepOut(ctypes.Structure):
                 ("stats", c_void_p)]
 
 
+class DlmTrace(ctypes.Structure):
+    _fields_ = [("layer", c_int32), ("qkv_cap", c_int32), ("h_in", c_void_p),
+                ("a_attn", c_void_p), ("qkv", c_void_p), ("q", c_void_p),
+                ("attn_out", c_void_p), ("h_mid", c_void_p), ("a_ffn", c_void_p),
+                ("act", c_void_p), ("h_out", c_void_p), ("u", c_void_p), ("logits", c_void_p),
+                ("qkv_splits", c_int32)]
+
+
+TRACE_BUFFERS = ("h_in", "a_attn", "qkv", "q", "attn_out", "h_mid", "a_ffn", "act", "h_out",
+                 "u", "logits")
+
+
 class DlmProfileEntry(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 32), ("calls", c_int32), ("total_ms", ctypes.c_double),
                 ("launches", c_int32)]
@@ -99,6 +111,8 @@ def lib():
                                         c_size_t, c_void_p]
         L.dlm_debug_logits.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), c_void_p,
                                        c_void_p, c_size_t, c_void_p]
+        L.dlm_debug_trace.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), POINTER(DlmTrace),
+                                      c_void_p, c_size_t, c_void_p]
         L.dlm_head_confidence.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p]
         L.dlm_profile_enable.argtypes = [c_void_p, c_int32, ctypes.c_char_p]
@@ -112,7 +126,8 @@ def lib():
         L.dlm_last_error.restype = ctypes.c_char_p
         for name in ["dlm_load_weights", "dlm_workspace_bytes", "dlm_kv_cache_alloc",
                      "dlm_cache_invalidate", "dlm_denoise_step", "dlm_cache_refresh",
-                     "dlm_debug_logits", "dlm_head_confidence", "dlm_profile_enable",
+                     "dlm_debug_logits", "dlm_debug_trace", "dlm_head_confidence",
+                     "dlm_profile_enable",
                      "dlm_profile_read", "dlm_profile_sample"]:
             getattr(L, name).restype = c_int32
         _lib = L
@@ -205,6 +220,22 @@ def debug_logits(model, cache, batch: DlmBatch, logits_out, workspace, stream=No
     check(lib().dlm_debug_logits(model, cache, ctypes.byref(batch), _ptr(logits_out),
                                  _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _stream(stream)))
+
+
+def debug_trace(model, cache, batch: DlmBatch, layer: int, buffers: dict, qkv_cap: int,
+                workspace, stream=None) -> int:
+    """Record layer `layer` of the step's forward into the given device tensors
+    (keys of TRACE_BUFFERS; missing keys record nothing). Returns the number of
+    QKV K-split slices written."""
+    unknown = set(buffers) - set(TRACE_BUFFERS)
+    if unknown:
+        raise ValueError(f"unknown trace buffers {sorted(unknown)}")
+    ptrs = [None if buffers.get(k) is None else buffers[k].data_ptr() for k in TRACE_BUFFERS]
+    tr = DlmTrace(layer, qkv_cap, *ptrs, 0)
+    check(lib().dlm_debug_trace(model, cache, ctypes.byref(batch), ctypes.byref(tr),
+                                _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                _stream(stream)))
+    return tr.qkv_splits
 
 
 def head_confidence(model, u_rows, m_rows: int, conf, tok, workspace, stream=None):

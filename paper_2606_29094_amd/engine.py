@@ -265,6 +265,67 @@ class Engine:
                 r.refreshed_block = r.block_start
         return out
 
+    def step_rows(self, reqs: List[Request], force_refresh: bool = False):
+        """[r0, r1) of the positions each request's next step recomputes, in
+        the packed row order of the step."""
+        rows = []
+        for r, d in zip(reqs, self.dlm_reqs(reqs, force_refresh)):
+            if d.flags & dlm.DLM_REQ_REFRESH:
+                rows.append((0, r.seq_len))
+            elif self.mode == "dual":
+                rows.append((r.block_start, r.block_start + r.block_len))
+            else:
+                rows.append((r.block_start, r.seq_len))
+        return rows
+
+    def debug_trace(self, reqs: List[Request], layer: int, logits: bool = True,
+                    qkv_cap: int = 8):
+        """Intermediates of layer `layer` of the forward of the step about to
+        run (dlm_debug_trace; cache writes as the step's), as device tensors,
+        plus the scaled logits and final-normed rows of every active-block
+        position when `logits`. Returns (buffers, QKV K-split slices)."""
+        sh = self.model.shape
+        dt = sh.torch_dtype
+        dreqs = self.dlm_reqs(reqs)
+        n = sum(r1 - r0 for r0, r1 in self.step_rows(reqs))
+        nblk = sum(d.block_len for d in dreqs)
+        qd = sh.n_q_heads * sh.head_dim
+        dev = self.device
+        e = lambda *shape, dtype=torch.float32: torch.empty(*shape, dtype=dtype, device=dev)
+        buf = {"h_in": e(n, sh.d_model), "a_attn": e(n, sh.d_model, dtype=dt),
+               "qkv": e(qkv_cap, n, sh.qkv_dim), "q": e(n, qd, dtype=dt),
+               "attn_out": e(n, qd, dtype=dt), "h_mid": e(n, sh.d_model),
+               "a_ffn": e(n, sh.d_model, dtype=dt), "act": e(n, sh.d_ffn, dtype=dt),
+               "h_out": e(n, sh.d_model)}
+        if logits:
+            buf["u"] = e(nblk, sh.d_model, dtype=dt)
+            buf["logits"] = e(nblk, sh.vocab)
+        batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id)
+        splits = dlm.debug_trace(self.model.handle, self.cache, batch, layer, buf, qkv_cap,
+                                 self.workspace)
+        for r, d in zip(reqs, dreqs):
+            if d.flags & dlm.DLM_REQ_REFRESH:
+                r.refreshed_block = r.block_start
+        buf["qkv"] = buf["qkv"][:splits]
+        return buf, splits
+
+    def read_kv(self, layer: int, slot: int, length: int):
+        """Keys and values of positions [0, length) of a slot at one layer, as
+        [length, n_kv_heads, head_dim] float tensors on the host, read from the
+        cache layout of dlm_kv_cache_alloc (per layer a key region
+        [slot][kv_head][pos][head_dim] then a value region
+        [slot][kv_head][head_dim][pos], slots of max_seq_len rounded up to 64)."""
+        sh = self.model.shape
+        dt = sh.torch_dtype
+        s_max = (self.max_seq_len + 63) // 64 * 64
+        per = self.n_slots * sh.n_kv_heads * s_max * sh.head_dim
+        region = self.cache_buf.view(dt)
+        k = region[(2 * layer) * per:(2 * layer + 1) * per].view(
+            self.n_slots, sh.n_kv_heads, s_max, sh.head_dim)[slot, :, :length]
+        v = region[(2 * layer + 1) * per:(2 * layer + 2) * per].view(
+            self.n_slots, sh.n_kv_heads, sh.head_dim, s_max)[slot, :, :, :length]
+        return (k.permute(1, 0, 2).float().cpu(), v.permute(2, 0, 1).float().cpu())
+
     def refresh(self, reqs: List[Request]):
         dreqs = self.dlm_reqs(reqs, force_refresh=True)
         batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id)

@@ -10,6 +10,7 @@ import torch
 import oracle
 import synth
 import synth.device as sdev
+from kernel_checks import check_head_unmask
 from paper_2606_29094_amd import engine
 
 # Tolerances: bf16 logits 2e-2, fp32 logits 1e-4 (max abs error over a row
@@ -27,9 +28,15 @@ CONF_TOL = 1e-3
 # checked against what the row's own logit error allows: if every scaled logit
 # of a row is within eta of the oracle's, S = sum exp(z - max z) moves by at
 # most a factor exp(2 eta), so |conf_gpu - conf_ref| <= conf_ref (exp(2 eta) - 1)
-# (plus the 1e-3 of the confidence computation itself). The logits must meet
-# LOGIT_TOL first; the tight 1e-3 bound alone is checked where the head's
-# inputs are identical (dlm_head_confidence).
+# (plus the 1e-3 of the confidence computation itself). This band is an extra
+# end-to-end check only: it is wide at full depth and does not bind the
+# 1e-3 confidence contract, which bf16 storage cannot meet end to end against
+# an fp64 oracle. What binds, on every step these helpers run: the logits
+# within LOGIT_TOL of the oracle's, and the fused head's confidences (1e-3)
+# and the unmask decisions (exact outside the 1e-3 bands) against the
+# oracle's confidence() and select_unmask() applied to the GPU's own logits of
+# the step (kernel_checks.check_head_unmask); each kernel on identical inputs
+# is checked in test_gpu_trace / test_gpu_configs.
 
 
 def conf_bound(conf_ref, eta):
@@ -154,7 +161,7 @@ def calibrated_inv_tau(cfg, W, oreqs, mode):
 def run_teacher_forced(cfg, W, eng, reqs, oreqs, mode, inv_tau, n_steps):
     """n_steps batched steps; before each, every request is set to the
     oracle's state; each request's step is compared with the oracle's."""
-    stats = {"lerr": 0.0, "cerr": 0.0, "exempt": 0, "kinds": []}
+    stats = {"lerr": 0.0, "cerr": 0.0, "exempt": 0, "kinds": [], "head": {}}
     for _ in range(n_steps):
         active = [i for i, oq in enumerate(oreqs) if not oq.done]
         if not active:
@@ -167,9 +174,12 @@ def run_teacher_forced(cfg, W, eng, reqs, oreqs, mode, inv_tau, n_steps):
             res = oracle.denoise_step(cfg, W, oreqs[i], mode, inv_tau, keep_logits=True)
             assert res.refresh == (flags[j] or mode == "none")
             stats["kinds"].append(res.refresh)
-            l, c, e = check_step_e2e(res, {k: v[j] for k, v in out.items()}, starts[j],
-                                     reqs[i].threshold, z_rows[j])
+            out_j = {k: v[j] for k, v in out.items()}
+            l, c, e = check_step_e2e(res, out_j, starts[j], reqs[i].threshold, z_rows[j])
+            check_head_unmask(z_rows[j], out_j, starts[j], res.masked_positions,
+                              reqs[i].threshold, stats["head"])
             stats["lerr"] = max(stats["lerr"], l)
             stats["cerr"] = max(stats["cerr"], c)
             stats["exempt"] += e
+    assert stats["head"].get("checked", 0) > 0, stats["head"]
     return stats

@@ -15,6 +15,7 @@ import torch
 import synth
 import synth.device as sdev
 from helpers import LOGIT_TOL, conf_bound, check_decisions
+from kernel_checks import check_head_unmask
 from paper_2606_29094_amd import engine
 
 pytestmark = pytest.mark.gpu
@@ -63,6 +64,20 @@ def _compare(gr, z_blk, out_r, blk_start):
     return rel.max(), cerr.max(), exempt
 
 
+def _head_all(z, out, starts, reqs):
+    """The fused head and the unmask decision of every request against the
+    oracle's confidence() / select_unmask() on the GPU's own logits of the
+    step (the whole block is masked at the first step)."""
+    counts, off = {}, 0
+    for j, r in enumerate(reqs):
+        L = r.block_len_at_start
+        check_head_unmask(z[off:off + L], {k: v[j] for k, v in out.items()}, starts[j],
+                          np.arange(starts[j], starts[j] + L), r.threshold, counts)
+        off += L
+    assert counts.get("checked", 0) > 0, counts
+    return counts
+
+
 def _run(model, cfg, workload, reqs_idx, mode):
     """Admit the requests, take the logits of the first step, then the step."""
     reqs = []
@@ -78,9 +93,12 @@ def _run(model, cfg, workload, reqs_idx, mode):
     for r, s in zip(reqs, saved):
         r.refreshed_block = s
     starts = [r.block_start for r in reqs]
+    for r in reqs:
+        r.block_len_at_start = r.block_len
     eng.step(reqs)
     out = eng.read_outputs(len(reqs))
     eng.close()
+    print("head + unmask on the GPU's own logits, every request:", _head_all(z, out, starts, reqs))
     return z, out, starts
 
 
@@ -93,7 +111,9 @@ def test_mha_nocache_step1_full_depth(mha_full):
 
 
 def test_mha_dual_batch8_step1_full_depth(mha_full):
-    """The whole 8-request batch (10240 recomputed rows); request 0 checked."""
+    """The whole 8-request batch (10240 recomputed rows): every request's head
+    and decisions on the GPU's logits; request 0 also against the stored
+    oracle values."""
     cfg, model, g = mha_full
     gr = [x for x in g["requests"] if x["workload"] == synth.C3_DUAL.name][0]
     z, out, starts = _run(model, cfg, synth.C3_DUAL, list(range(8)), "dual")
@@ -115,7 +135,7 @@ def test_gqa_dual_step1_full_depth(gpu):
     cfg = synth.GQA_7B
     t = sdev.model_tensors(cfg)
     model = engine.DeviceModel(engine.ModelShape.of(cfg), t, g["inv_tau"])
-    z, out, starts = _run(model, cfg, synth.C5, [0, 1, 2, 3], "dual")
+    z, out, starts = _run(model, cfg, synth.C5, list(range(64)), "dual")
     off = 0
     for j, gr in enumerate(g["requests"]):
         blk = z[off:off + synth.C5.block]

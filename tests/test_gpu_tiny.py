@@ -69,9 +69,15 @@ def _compare_step(res, out_r, blk_start, gamma, logits_tol_gap=1e-4):
     near = set(A[np.abs(res.masked_conf - gamma) <= CONF_TOL].tolist())
     forced = not np.any(res.masked_conf > gamma)
     if forced:
+        # nothing passes: exactly one position is unmasked, the most confident
+        # one; when the top confidences are within the tolerance, any of the
+        # tied top positions
+        assert n == 1, (n, sorted(got))
         c = np.sort(res.masked_conf)[::-1]
         if len(c) > 1 and c[0] - c[1] <= CONF_TOL:
-            return 1   # position may differ: exempt
+            tied = set(A[res.masked_conf >= c[0] - 2 * CONF_TOL].tolist())
+            assert got <= tied, (sorted(got), sorted(tied))
+            return 1
         assert got == want
         return 0
     assert (got ^ want) <= near, (got, want)
@@ -103,7 +109,7 @@ def test_trajectory_teacher_forced_and_golden(tiny):
         steps += 1
     assert steps == g["n_steps"]
     assert oreq.tokens.tolist() == g["final_tokens"]
-    print("tiny trajectory steps", steps, "exempt", exempt)
+    print("tiny trajectory steps", steps, "tied-top forced steps", exempt)
 
 
 def test_free_running_generation_matches_golden(tiny):
@@ -119,10 +125,13 @@ def test_free_running_generation_matches_golden(tiny):
         assert n <= G
     toks, mask = eng.read_state(r)
     assert not mask.any()
-    agree = np.mean(toks == np.array(g["final_tokens"]))
-    print("free-running: steps", n, "golden", g["n_steps"], "token agreement", agree)
-    # free running may diverge only through exempt (near-tie) decisions
-    assert n == g["n_steps"] or agree > 0.9
+    print("free-running: steps", n, "golden", g["n_steps"])
+    # the stored trajectory's decisions are all outside the 1e-3 bands except
+    # forced steps among tied top confidences, where the GPU and the oracle
+    # pick the same position (checked step by step in the teacher-forced
+    # test), so the free-running generation is the stored one
+    assert n == g["n_steps"]
+    assert toks.tolist() == g["final_tokens"]
 
 
 def test_step_is_deterministic(tiny):

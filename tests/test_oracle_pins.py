@@ -363,6 +363,63 @@ def test_stale_cache_is_an_approximation():
     assert not np.allclose(res_c.logits, res_n.logits, rtol=1e-6)
 
 
+def test_prefix_cache_recomputes_the_suffix_and_dual_keeps_it():
+    """Prefix vs dual caching (paper, "Support for Approximate Caching": the
+    keys/values of the prompt, completed blocks and still-masked suffix blocks
+    are reused while a block is denoised). Prefix mode recomputes the active
+    block and every later position, dual mode the active block only.
+
+    With an empty prompt the prefix cache step of block 0 therefore reads no
+    cached row at all and must equal the no-cache step exactly, while the dual
+    step reads the suffix as the refresh wrote it and must differ. With a
+    prompt, after the block changed, the prefix step rewrites the suffix cache
+    rows of every layer past the first (they depend on the changed block),
+    dual leaves them as the refresh wrote them, both leave the rows before the
+    block untouched, and their logits differ."""
+    import copy
+    cfg = TINY
+    W = _weights(cfg, scale=8.0)
+    inv_tau = 20.0
+    # empty prompt: prefix step == no-cache step bit for bit, dual differs
+    base = _fresh(cfg, 0, 12, 4, 0.0)
+    oracle.step_forward(cfg, W, base, "prefix", refresh=True)
+    base.tokens[1:3] = [3, 4]
+    base.mask[1:3] = False
+    res = {}
+    for mode in ("none", "prefix", "dual"):
+        r = copy.deepcopy(base)
+        h, rows, refresh = oracle.step_forward(cfg, W, r, mode)
+        assert refresh == (mode == "none")
+        res[mode] = (oracle.finish_step(cfg, W, r, h, rows, refresh, inv_tau,
+                                        keep_logits=True), rows)
+    assert res["prefix"][1] == (0, 12) and res["dual"][1] == (0, 4)
+    assert np.array_equal(res["prefix"][0].logits, res["none"][0].logits)
+    assert not np.allclose(res["dual"][0].logits, res["none"][0].logits, rtol=1e-6)
+
+    # with a prompt: which cache rows each mode rewrites
+    P, G, B = 9, 12, 4
+    req = _fresh(cfg, P, G, B, 0.0)
+    oracle.step_forward(cfg, W, req, "prefix", refresh=True)
+    ref_k = [k.copy() for k in req.cache_k]
+    req.tokens[P:P + 2] = [5, 6]
+    req.mask[P:P + 2] = False
+    s, e = P, P + B
+    out = {}
+    for mode in ("prefix", "dual"):
+        r = copy.deepcopy(req)
+        h, rows, refresh = oracle.step_forward(cfg, W, r, mode)
+        assert not refresh
+        out[mode] = (r, oracle.finish_step(cfg, W, r, h, rows, refresh, inv_tau,
+                                           keep_logits=True))
+    for l in range(W.n_layers):
+        for mode in ("prefix", "dual"):
+            assert np.array_equal(out[mode][0].cache_k[l][:s], ref_k[l][:s])
+        assert np.array_equal(out["dual"][0].cache_k[l][e:], ref_k[l][e:])
+        if l >= 1:
+            assert not np.allclose(out["prefix"][0].cache_k[l][e:], ref_k[l][e:], rtol=1e-9)
+    assert not np.allclose(out["prefix"][1].logits, out["dual"][1].logits, rtol=1e-6)
+
+
 @pytest.mark.parametrize("mode", ["none", "dual", "prefix"])
 def test_threshold_one_unmasks_one_per_step(mode):
     cfg = TINY
