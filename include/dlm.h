@@ -66,7 +66,8 @@ enum {
   DLM_MAX_BLOCK = 64,     /* largest block length (one 64-lane wavefront per request) */
   DLM_MAX_REQ = 64,       /* largest number of requests in one step                     */
   DLM_MAX_SEQ = 8192,     /* largest sequence length                                    */
-  DLM_NSTATS = 8          /* confidence statistics per request (dlm_step_out.stats)    */
+  DLM_NSTATS = 8,         /* confidence statistics per request (dlm_step_out.stats)    */
+  DLM_SCRATCH_BYTES = 134217728 /* scratch of dlm_denoise_step_noalloc (128 MiB per GPU)  */
 };
 
 /* Request flag: this step is a recompute step (whole sequence, cache rewritten). */
@@ -199,6 +200,26 @@ dlm_status dlm_cache_invalidate(dlm_cache* c, int32_t slot);
 dlm_status dlm_denoise_step(dlm_model* m, dlm_cache* c, const dlm_batch* b,
                             const float* thresholds, const dlm_step_out* out,
                             void* workspace, size_t ws_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the step of
+ * dlm_denoise_step with no workspace argument. Its scratch is a fixed array
+ * of DLM_SCRATCH_BYTES (128 MiB) built into the library, one per GPU the
+ * library runs on, held until the process ends; the first call on a device
+ * looks up that device's copy. A step whose workspace (dlm_workspace_bytes
+ * for its rows and requests) exceeds DLM_SCRATCH_BYTES is rejected with
+ * DLM_ESIZE before anything is enqueued (for example the 512-row step of a
+ * 4096-wide, 32-layer bf16 model fits, a 1024-row step does not). The call
+ * allocates nothing: no hipMalloc, no hipFree, no allocating library routine.
+ * Every call on one GPU shares that GPU's array, which keeps the previous
+ * call's contents (the step needs nothing in it to start at zero); calls that
+ * overlap on one GPU (different streams, or threads without ordering between
+ * them) race on it and must be serialised by the caller. Kernel timing
+ * (dlm_profile_enable) does not apply to this entry point. Arguments,
+ * outputs, cache rules and errors are those of dlm_denoise_step. */
+dlm_status dlm_denoise_step_noalloc(dlm_model* m, dlm_cache* c, const dlm_batch* b,
+                                    const float* thresholds, const dlm_step_out* out,
+                                    void* stream);
 
 /* Recompute step without unmasking (paper: "Implementation", the caches are
  * rebuilt during recompute steps; "Request Scheduling", a request migrates or

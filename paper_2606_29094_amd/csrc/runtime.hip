@@ -9,6 +9,7 @@
 #include <cstdint>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -45,6 +46,37 @@ dlm_status fail(dlm_status s, const char* fmt, ...) {
   } while (0)
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace
+
+// Scratch of dlm_denoise_step_noalloc: one copy per device, in the library's
+// code object. Host code never uses this name as an address: the device
+// address of each GPU's copy comes from hipGetSymbolAddress (scratch_address).
+static __device__ __align__(256) char scratch[DLM_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch, looked up once per device.
+dlm_status scratch_address(void** out) {
+  int dev = 0;
+  HIPCHECK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(DLM_EUNSUPPORTED, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIPCHECK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p || reinterpret_cast<uintptr_t>(p) % 256 != 0)
+      return fail(DLM_EHIP, "scratch of device %d is not 256-byte aligned", dev);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DLM_OK;
+}
 
 }  // namespace
 
@@ -640,6 +672,39 @@ dlm_status dlm_denoise_step(dlm_model* m, dlm_cache* c, const dlm_batch* b,
   s = check_ws(m, p, workspace, ws_bytes, &L);
   if (s != DLM_OK) return s;
   s = dispatch(m, c, b, p, L, workspace, Tail::Unmask, out, nullptr, stream);
+  if (s == DLM_OK) mark_refreshed(c, b, false);
+  return s;
+}
+
+dlm_status dlm_denoise_step_noalloc(dlm_model* m, dlm_cache* c, const dlm_batch* b,
+                                    const float* thresholds, const dlm_step_out* out,
+                                    void* stream) {
+  g_err.clear();
+  dlm_status s = check_handles(m, c);
+  if (s != DLM_OK) return s;
+  if (!thresholds) return fail(DLM_EINVAL, "thresholds is NULL");
+  if (!out || !out->n_unmasked || !out->pos || !out->tok || !out->conf)
+    return fail(DLM_EINVAL, "step output pointer is NULL");
+  if (out->stats && (!b || !b->tok_conf))
+    return fail(DLM_EINVAL, "confidence statistics need batch.tok_conf");
+  StepPlan p;
+  s = make_plan(m, c, b, thresholds, false, &p);
+  if (s != DLM_OK) return s;
+  const size_t need = layout(m, p.n_rows, p.n_req).total;
+  if (need > (size_t)DLM_SCRATCH_BYTES)
+    return fail(DLM_ESIZE, "this step needs %zu bytes of scratch (%d rows); the fixed scratch "
+                "holds %zu", need, p.n_rows, (size_t)DLM_SCRATCH_BYTES);
+  void* ws = nullptr;
+  s = scratch_address(&ws);
+  if (s != DLM_OK) return s;
+  Layout L;
+  s = check_ws(m, p, ws, (size_t)DLM_SCRATCH_BYTES, &L);
+  if (s != DLM_OK) return s;
+  // no kernel timing here (its events would be created on first use)
+  const bool prof_on = m->prof.on;
+  m->prof.on = false;
+  s = dispatch(m, c, b, p, L, ws, Tail::Unmask, out, nullptr, stream);
+  m->prof.on = prof_on;
   if (s == DLM_OK) mark_refreshed(c, b, false);
   return s;
 }

@@ -19,12 +19,14 @@ DLM_F32, DLM_BF16 = 0, 1
 DLM_CACHE_NONE, DLM_CACHE_PREFIX, DLM_CACHE_DUAL = 0, 1, 2
 DLM_MAX_BLOCK, DLM_MAX_REQ, DLM_MAX_SEQ = 64, 64, 8192
 DLM_NSTATS = 8
+DLM_SCRATCH_BYTES = 128 << 20
 DLM_REQ_REFRESH = 1
 MODES = {"none": DLM_CACHE_NONE, "prefix": DLM_CACHE_PREFIX, "dual": DLM_CACHE_DUAL}
 
 EXPORTS = ["dlm_load_weights", "dlm_model_destroy", "dlm_workspace_bytes",
            "dlm_kv_cache_alloc", "dlm_cache_destroy", "dlm_cache_invalidate",
-           "dlm_denoise_step", "dlm_cache_refresh", "dlm_debug_logits", "dlm_debug_trace",
+           "dlm_denoise_step", "dlm_denoise_step_noalloc", "dlm_cache_refresh",
+           "dlm_debug_logits", "dlm_debug_trace",
            "dlm_head_confidence", "dlm_profile_enable", "dlm_profile_read",
            "dlm_profile_sample", "dlm_ceiling_mfma", "dlm_ceiling_copy", "dlm_last_error"]
 
@@ -107,6 +109,8 @@ def lib():
         L.dlm_cache_invalidate.argtypes = [c_void_p, c_int32]
         L.dlm_denoise_step.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), POINTER(c_float),
                                        POINTER(DlmStepOut), c_void_p, c_size_t, c_void_p]
+        L.dlm_denoise_step_noalloc.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch),
+                                               POINTER(c_float), POINTER(DlmStepOut), c_void_p]
         L.dlm_cache_refresh.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), c_void_p,
                                         c_size_t, c_void_p]
         L.dlm_debug_logits.argtypes = [c_void_p, c_void_p, POINTER(DlmBatch), c_void_p,
@@ -125,7 +129,8 @@ def lib():
         L.dlm_last_error.argtypes = []
         L.dlm_last_error.restype = ctypes.c_char_p
         for name in ["dlm_load_weights", "dlm_workspace_bytes", "dlm_kv_cache_alloc",
-                     "dlm_cache_invalidate", "dlm_denoise_step", "dlm_cache_refresh",
+                     "dlm_cache_invalidate", "dlm_denoise_step", "dlm_denoise_step_noalloc",
+                     "dlm_cache_refresh",
                      "dlm_debug_logits", "dlm_debug_trace", "dlm_head_confidence",
                      "dlm_profile_enable",
                      "dlm_profile_read", "dlm_profile_sample"]:
@@ -209,6 +214,14 @@ def denoise_step(model, cache, batch: DlmBatch, thresholds, out: DlmStepOut, wor
     check(lib().dlm_denoise_step(model, cache, ctypes.byref(batch), thr, ctypes.byref(out),
                                  _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _stream(stream)))
+
+
+def denoise_step_noalloc(model, cache, batch: DlmBatch, thresholds, out: DlmStepOut,
+                         stream=None):
+    """dlm_denoise_step with the library's fixed scratch instead of a workspace."""
+    thr = (c_float * batch.n_req)(*[float(t) for t in thresholds])
+    check(lib().dlm_denoise_step_noalloc(model, cache, ctypes.byref(batch), thr,
+                                         ctypes.byref(out), _stream(stream)))
 
 
 def cache_refresh(model, cache, batch: DlmBatch, workspace, stream=None):
