@@ -1,18 +1,22 @@
 #!/usr/bin/env python3
 """Denoising-step throughput on one MI355X.
 
-Default workload: the bf16 MHA model shaped like LLaDA-8B (32 layers, d 4096,
-32 heads of 128, SwiGLU 12288, vocab 126464; synthetic N(0, 0.02) weights),
-batch 1, 256 random prompt tokens + 256 [MASK] tokens decoded in blocks of 32,
-no cache (every step recomputes all 512 positions), threshold 0.9, logits
-scaled by the calibrated 1/tau. One step = one dlm_denoise_step call (the whole
-hot path: embedding, every layer, fused LM head and confidence, unmask) plus
-the per-step read-back of the unmask counts. A finished request is replaced at
-once (the same prompt again, or the slot's next request for the heterogeneous
-workload), so the batch stays full.
+Default workload: the largest single-GPU configuration, the bf16 GQA model
+shaped like Dream-7B (28 layers, d 3584, 28 query / 4 key-value heads of 128,
+SwiGLU 18944, vocab 152064; synthetic N(0, 0.02) weights), batch 64, each
+request 512 random prompt tokens + 512 [MASK] tokens decoded in blocks of 64
+with a dual KV cache (the first step of every block recomputes the whole
+sequence and rewrites the request's cache, the other steps recompute the
+block only), threshold 0.9, logits scaled by the calibrated 1/tau. One step =
+one dlm_denoise_step call over the whole batch (embedding, every layer, fused
+LM head and confidence, unmask) plus the per-step read-back of the unmask
+counts. A finished request is replaced at once (the same prompt again, or the
+slot's next request for the heterogeneous workload), so the batch stays full
+and requests at different blocks mix recompute and cache steps in one step.
 
---workload selects the other configurations (batch 8 with prefix or dual
-cache, the heterogeneous batch of 32, the GQA batch of 64).
+--workload selects the other configurations (the single-request no-cache
+step of the MHA model, batch 8 with prefix or dual cache, the heterogeneous
+batch of 32).
 
 Prints one JSON line: steps/s (value), unmasked tokens/s, the roofline of the
 dominant kernel (in-library HIP events on the launch stream over the timed
@@ -43,12 +47,13 @@ def load_inv_tau(model_name: str):
         return float(json.load(f)["inv_tau"]), os.path.relpath(path, ROOT)
 
 
-def measured_traffic(kernel_class: str):
-    """HBM bytes per launch of a kernel class from the committed rocprofv3 counter
-    summary (profiles/traffic_<class>.json), or None when there is none or the
-    kernel's sources changed since the counters were taken."""
+def measured_traffic(kernel_class: str, workload: str):
+    """HBM bytes per launch of a kernel class on a workload from the committed
+    rocprofv3 counter summary (profiles/traffic_<class>_<workload>.json), or
+    None when there is none or the kernel's sources changed since the counters
+    were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}_{workload}.json")
     if not os.path.exists(path):
         return None, None
     with open(path) as f:
@@ -110,12 +115,22 @@ def step_work(shape, rows, m_rows):
     return F, B
 
 
-def cpu_baseline(cfg, tensors, prompt, G, block, inv_tau, n_sample_layers):
-    """Time the oracle (fp64 NumPy) on a bounded sample of one no-cache step of
-    one request: the first n_sample_layers layers over all rows plus the LM head
-    and confidence of the block's masked rows; scaled to a whole step (layer time
-    x n_layers / n)."""
+def cpu_baseline(cfg, tensors, w, inv_tau, n_sample_layers, n_sample_reqs, rows_per_step,
+                 masked_per_step):
+    """Time the oracle (fp64 NumPy) on a bounded sample of the workload's step and
+    scale it to one step of the timed region.
+
+    The sample: the rows the workload's steady step recomputes for
+    n_sample_reqs requests (the whole sequence without a cache; the active
+    block with a dual cache; block and suffix with a prefix cache; keys over
+    the whole slot) through the first n_sample_layers layers, plus the LM head
+    and confidence of their block rows. The oracle's cost is linear in the
+    recomputed rows (every row attends over its whole slot), so the step time
+    is (layer time per sampled row) x (recomputed rows per timed step) x
+    n_layers / n_sample_layers + (head time per row) x (masked rows per timed
+    step)."""
     import oracle
+    import synth
     try:
         from threadpoolctl import threadpool_info
         threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
@@ -138,30 +153,51 @@ def cpu_baseline(cfg, tensors, prompt, G, block, inv_tau, n_sample_layers):
     W = oracle.Weights({"embed": f(tensors["embed"]), "lm_head": f(tensors["lm_head"]),
                         "final_norm": f(tensors["final_norm"])}, layer_fn=host_layer,
                        n_layers=n_sample_layers)
-    req = oracle.Request.new(prompt, G, block, 0.9, cfg.mask_id)
-    L = req.seq_len
-    oracle.ensure_cache(cfg, req, n_sample_layers)
-    t0 = time.perf_counter()
-    h = oracle.embed_rows(cfg, W, req, 0, L)
-    t_layers = time.perf_counter() - t0
+    mode = w.cache_mode
+    reqs, rows, hs = [], [], []
+    t_layers = 0.0
+    for i in range(n_sample_reqs):
+        prompt, G, _ = synth.request(w, i)
+        prompt = prompt % cfg.vocab
+        req = oracle.Request.new(prompt, G, w.block, 0.9, cfg.mask_id)
+        oracle.ensure_cache(cfg, req, n_sample_layers)
+        # the mode's steady step: a cache step of block 0 (its cached rows are
+        # what the last recompute step wrote; their values do not change the
+        # cost), or the whole sequence without a cache
+        r0, r1 = oracle.recompute_rows(req, mode, mode == "none")
+        t0 = time.perf_counter()
+        hs.append(oracle.embed_rows(cfg, W, req, r0, r1))
+        t_layers += time.perf_counter() - t0
+        reqs.append(req)
+        rows.append((r0, r1))
     for l in range(n_sample_layers):
         Wl = W.layer(l)
         ta = time.perf_counter()
-        h = oracle.layer_forward(cfg, Wl, h, 0, L, req.cache_k[l], req.cache_v[l])
+        for i, req in enumerate(reqs):
+            hs[i] = oracle.layer_forward(cfg, Wl, hs[i], rows[i][0], rows[i][1],
+                                         req.cache_k[l], req.cache_v[l])
         t_layers += time.perf_counter() - ta
         del Wl
     t1 = time.perf_counter()
-    s, e = req.block_bounds
-    z = oracle.head_logits(cfg, W, h[s:e], inv_tau)
-    conf, tok = oracle.confidence(z)
-    oracle.select_unmask(conf, 0.9)
+    n_head = 0
+    for req, h, (r0, _) in zip(reqs, hs, rows):
+        s, e = req.block_bounds
+        z = oracle.head_logits(cfg, W, h[s - r0:e - r0], inv_tau)
+        conf, tok = oracle.confidence(z)
+        oracle.select_unmask(conf, 0.9)
+        n_head += e - s
     t_head = time.perf_counter() - t1
-    t_step = t_layers * cfg.n_layers / n_sample_layers + t_head
+    n_rows = sum(b - a for a, b in rows)
+    t_step = (t_layers / n_rows * rows_per_step * cfg.n_layers / n_sample_layers
+              + t_head / n_head * masked_per_step)
     return {"value": 1.0 / t_step, "unit": "steps/s",
             "cores": len(os.sched_getaffinity(0)), "blas_threads": threads, "kind": "oracle",
-            "sample": (f"{n_sample_layers} of {cfg.n_layers} layers of one no-cache step "
-                       f"({L} rows, fp64 NumPy) + LM head/confidence of {e - s} rows; layer "
-                       f"time scaled x{cfg.n_layers}/{n_sample_layers}"),
+            "sample": (f"{n_sample_reqs} request(s) x {n_rows // n_sample_reqs} recomputed rows "
+                       f"({mode}-cache steady step, fp64 NumPy) through {n_sample_layers} of "
+                       f"{cfg.n_layers} layers + LM head/confidence of {n_head} rows; "
+                       f"extrapolated linearly to the timed steps' mean of {rows_per_step:.0f} "
+                       f"recomputed and {masked_per_step:.0f} masked rows per step over all "
+                       f"layers"),
             "measured_s": t_layers + t_head}
 
 
@@ -270,11 +306,15 @@ def main():
                     help="timed steps (default 40; 256 for c4)")
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed warm-up steps (default 5; 64 for c4)")
-    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="c5", choices=sorted(WORKLOADS))
     ap.add_argument("--threshold", type=float, default=None,
                     help="override every request's threshold (the GQA sweep)")
-    ap.add_argument("--cpu-layers", type=int, default=24,
-                    help="layers of the CPU oracle sample (0 disables the CPU baseline)")
+    ap.add_argument("--cpu-layers", type=int, default=None,
+                    help="layers of the CPU oracle sample (0 disables the CPU baseline; default: "
+                         "24 for the single-request no-cache workload, every layer otherwise)")
+    ap.add_argument("--cpu-requests", type=int, default=None,
+                    help="requests of the CPU oracle sample (default: 1 without a cache, 4 "
+                         "with one)")
     ap.add_argument("--inv-tau", type=float, default=None,
                     help="override the stored calibrated 1/tau")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -505,8 +545,7 @@ def main():
         F, Bb = stats["cls"][dom]
         F1, B1 = F / launches, Bb / launches           # per launch
         avg_s = tot / calls * 1e-3
-        traffic, traffic_src = (measured_traffic(dom) if args.workload == "c2" and tp == 1
-                                else (None, None))
+        traffic, traffic_src = (measured_traffic(dom, w.name) if tp == 1 else (None, None))
         if F1 / B1 >= ridge:
             achieved = F1 / avg_s / 1e12
             roof = {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": peak,
@@ -528,14 +567,13 @@ def main():
                  "flop_per_step": Fs, "bytes_per_step": Bs}
 
     cpu = None
-    if args.cpu_layers > 0:
-        prompt, G, _ = synth.request(w, 0)
-        if tp > 1:
-            prompt = prompt % cfg.vocab
-        cpu = cpu_baseline(cfg, tensors, prompt, G, w.block, inv_tau, args.cpu_layers)
-        if B > 1 or w.cache_mode != "none":
-            cpu["sample"] += ("; one request's no-cache step (the timed GPU steps batch "
-                              f"{B} requests, cache mode {w.cache_mode})")
+    cpu_layers = args.cpu_layers
+    if cpu_layers is None:
+        cpu_layers = min(24, cfg.n_layers) if w.cache_mode == "none" else cfg.n_layers
+    if cpu_layers > 0:
+        n_req = args.cpu_requests or (1 if w.cache_mode == "none" else 4)
+        cpu = cpu_baseline(cfg, tensors, w, inv_tau, min(cpu_layers, cfg.n_layers), n_req,
+                           stats["rows"] / args.steps, stats["masked"] / args.steps)
 
     lat, dist = step_breakdown(stats["per_step"])
     rs = stats["req_steps"]
@@ -571,6 +609,7 @@ def main():
                    "avg_refresh_requests": stats["refresh_reqs"] / args.steps,
                    "confidence_stats": bool(args.stats)},
         "roofline": roof,
+        "class_work": {k: {"flop": f, "bytes": bb} for k, (f, bb) in stats["cls"].items()},
         "step_roofline": step_roof,
         "step_latency": lat,
         "step_distribution": dist,
