@@ -23,10 +23,14 @@ Supporting Approximate KV Caching", Algorithms 5 and 6):
   sizes times the SLO (Alg. 2); with caching, the throughput of a block made
   of block-size - 1 cache steps at the largest batch and one recompute step
   of an average request (Alg. 5);
-* load control walks the requests in arrival order and, for each, drops
-  candidate thresholds from the top while the committed load plus this
-  request's load plus every later request's load at the lowest threshold
-  would exceed capacity; the lowest threshold is always kept (Alg. 2).
+* load control gives each request, in arrival order, the highest maximum
+  threshold for which the worst-case aggregate load (earlier requests at
+  their maxima, this one at the candidate, later ones at the lowest
+  threshold) fits the capacity; the lowest threshold is always kept (Alg. 2).
+
+Both choices are written from the prose of those sections as set
+definitions (the highest fitting candidate, the largest feasible maximum),
+not by transcribing the printed loops.
 
 Readings (the paper gives the latency profile as a table over batch sizes):
 the latency at a token count between measured points is linear between its
@@ -102,11 +106,13 @@ def predicted_time_left(p: Params, inst: Instance, req: Req, gi: int) -> float:
 
 
 def update_conf_threshold(p: Params, inst: Instance, req: Req) -> int:
-    """Alg. 1: the highest allowed candidate meeting the remaining budget."""
-    for gi in sorted(req.allowed, reverse=True):
-        req.gamma_idx = gi
-        if predicted_time_left(p, inst, req, gi) <= req.slo_left_s:
-            break
+    """The threshold choice of "SLO-aware Confidence Threshold Adjustment":
+    among the allowed candidates, the highest one whose predicted remaining
+    time fits the request's remaining SLO budget; when none fits, the lowest
+    allowed one (the paper's loop over the allowed candidates from the top
+    ends there)."""
+    fits = [gi for gi in req.allowed if predicted_time_left(p, inst, req, gi) <= req.slo_left_s]
+    req.gamma_idx = max(fits) if fits else min(req.allowed)
     return req.gamma_idx
 
 
@@ -136,18 +142,19 @@ def cluster_capacity(p: Params, profiles: Sequence[Profile], tokens_per_req: flo
 
 
 def update_allowed(p: Params, reqs: List[Req], capacity: float) -> None:
-    """Alg. 2: requests in arrival order (the list order)."""
-    n = len(reqs)
-    g_min = 0
-    min_remain = [0.0] * n
-    for i in range(n - 2, -1, -1):
-        min_remain[i] = min_remain[i + 1] + req_load(p, reqs[i + 1], g_min)
-    used = 0.0
+    """Load control of "Adaptive Load Control", requests in arrival order (the
+    list order): each request gets the highest maximum threshold for which
+    the worst-case aggregate load fits the capacity, the worst case being
+    every earlier request at the maximum it was given, this request at the
+    candidate and every later request at the lowest threshold. The lowest
+    threshold stays allowed even when it does not fit. A request's allowed
+    set is every candidate up to its maximum."""
+    maxima: List[int] = []
     for i, req in enumerate(reqs):
-        req.allowed = list(range(len(p.gammas)))
-        for gi in range(len(p.gammas) - 1, -1, -1):
-            load = req_load(p, req, gi)
-            if used + load + min_remain[i] <= capacity or gi == g_min:
-                used += load
-                break
-            req.allowed.remove(gi)
+        earlier = sum(req_load(p, reqs[j], maxima[j]) for j in range(i))
+        later = sum(req_load(p, reqs[j], 0) for j in range(i + 1, len(reqs)))
+        fits = [gi for gi in range(len(p.gammas))
+                if earlier + req_load(p, req, gi) + later <= capacity]
+        top = max(fits) if fits else 0
+        maxima.append(top)
+        req.allowed = list(range(top + 1))

@@ -27,14 +27,9 @@
 #include "common.h"
 #include "kernels.h"
 
-#ifndef ATTN_PLO
-#define ATTN_PLO 1
-#endif
-
 namespace dlm {
 
 constexpr int kKeyTile = 64;
-constexpr bool kPLo = ATTN_PLO;
 
 // Wave layout: QG query groups of 16 rows x KG key groups. A block stages
 // key tiles of 64 * KG positions; key group kg works on keys [64 kg, 64 kg +
@@ -47,9 +42,9 @@ constexpr bool kPLo = ATTN_PLO;
 // m is only moved (and l, O^T rescaled) when a tile's maximum exceeds it by
 // more than 8 / c, so the weights stay below 2^8 and most tiles skip the
 // rescale; the normalised result is the same.
-// PLO: P is fed to the PV product as two bf16 terms (P = P_hi + P_lo, about
+// P is fed to the PV product as two bf16 terms (P = P_hi + P_lo, about
 // 16 significant bits, two MFMAs per block) instead of one.
-template <int DH, int QG, int KG, bool PLO>
+template <int DH, int QG, int KG>
 __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, const bf16* __restrict__ q,
                                                                const bf16* __restrict__ kc,
                                                                const bf16* __restrict__ vc,
@@ -242,14 +237,14 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
       for (int e = 0; e < 8; ++e) {
         const float pv = e < 4 ? sblk[2 * j][e] : sblk[2 * j + 1][e - 4];
         ph[e] = (bf16)pv;
-        if constexpr (PLO) pl[e] = (bf16)(pv - (float)ph[e]);
+        pl[e] = (bf16)(pv - (float)ph[e]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const bf16* vrow = vs + (db * 16 + (lane & 15)) * VS + kg * 64 + 32 * j + 8 * g;
         const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vrow));
         o[db] = mfma16_bf16(a, ph, o[db]);
-        if constexpr (PLO) o[db] = mfma16_bf16(a, pl, o[db]);
+        o[db] = mfma16_bf16(a, pl, o[db]);
       }
     }
     if (t + 1 < ntiles) {
@@ -336,7 +331,7 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
 // Keys at or beyond L inside the last tile are read from the slot (a slot
 // holds s_max positions, a multiple of 64) and then masked: their scores are
 // set to -inf and their V^T entries cleared in LDS.
-template <int DH, int GH, int QG, bool PLO>
+template <int DH, int GH, int QG>
 __global__ __launch_bounds__(GH* QG * 64) void attn_gqa_kernel(StepPlan p, const bf16* __restrict__ q,
                                                              const bf16* __restrict__ kc,
                                                              const bf16* __restrict__ vc,
@@ -529,14 +524,14 @@ __global__ __launch_bounds__(GH* QG * 64) void attn_gqa_kernel(StepPlan p, const
       for (int e = 0; e < 8; ++e) {
         const float pv = e < 4 ? sblk[2 * j][e] : sblk[2 * j + 1][e - 4];
         ph[e] = (bf16)pv;
-        if constexpr (PLO) pl[e] = (bf16)(pv - (float)ph[e]);
+        pl[e] = (bf16)(pv - (float)ph[e]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const u32x4 a = *reinterpret_cast<const u32x4*>(vst + (db * 16 + (lane & 15)) * 128 +
                                                         (((4 * j + g) << 4) ^ sw));
         o[db] = mfma16_bf16(__builtin_bit_cast(bf16x8, a), ph, o[db]);
-        if constexpr (PLO) o[db] = mfma16_bf16(__builtin_bit_cast(bf16x8, a), pl, o[db]);
+        o[db] = mfma16_bf16(__builtin_bit_cast(bf16x8, a), pl, o[db]);
       }
     }
   }
@@ -619,7 +614,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(StepPlan p, const float* _
   }
 }
 
-template <int DH, int QG, int KG, bool PLO>
+template <int DH, int QG, int KG>
 static hipError_t launch_attn(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
                               int s_max, int hq, int hkv, bf16* out, float scale_log2,
                               hipStream_t st) {
@@ -627,12 +622,12 @@ static hipError_t launch_attn(const StepPlan& p, const bf16* q, const bf16* kc, 
   int tiles = 0;
   for (int r = 0; r < p.n_req; ++r) tiles += (p.r[r].nrows + QT - 1) / QT;
   if (tiles == 0) return hipSuccess;
-  DLM_LAUNCH((attn_bf16_kernel<DH, QG, KG, PLO>), dim3(hq, tiles), dim3(QG * KG * 64), 0, st,
+  DLM_LAUNCH((attn_bf16_kernel<DH, QG, KG>), dim3(hq, tiles), dim3(QG * KG * 64), 0, st,
                      p, q, kc, vc, s_max, hq, hkv, out, scale_log2);
   return hipGetLastError();
 }
 
-template <int DH, int GH, int QG, bool PLO>
+template <int DH, int GH, int QG>
 static hipError_t launch_gqa(const StepPlan& p, const bf16* q, const bf16* kc, const bf16* vc,
                              int s_max, int hq, int hkv, bf16* out, float scale_log2,
                              hipStream_t st) {
@@ -640,7 +635,7 @@ static hipError_t launch_gqa(const StepPlan& p, const bf16* q, const bf16* kc, c
   int tiles = 0;
   for (int r = 0; r < p.n_req; ++r) tiles += (p.r[r].nrows + QT - 1) / QT;
   if (tiles == 0) return hipSuccess;
-  DLM_LAUNCH((attn_gqa_kernel<DH, GH, QG, PLO>), dim3(hkv * tiles), dim3(GH * QG * 64), 0,
+  DLM_LAUNCH((attn_gqa_kernel<DH, GH, QG>), dim3(hkv * tiles), dim3(GH * QG * 64), 0,
                      st, p, q, kc, vc, s_max, hq, hkv, tiles, out, scale_log2);
   return hipGetLastError();
 }
@@ -652,10 +647,10 @@ static hipError_t attention_dh(const StepPlan& p, const bf16* q, const bf16* kc,
                                int s_max, int hq, int hkv, bf16* out, float scale_log2,
                                hipStream_t st) {
   switch (hkv > 0 && hq % hkv == 0 ? hq / hkv : 0) {
-    case 2: return launch_gqa<DH, 2, 4, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
-    case 4: return launch_gqa<DH, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
-    case 7: return launch_gqa<DH, 7, 1, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
-    case 8: return launch_gqa<DH, 8, 1, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    case 2: return launch_gqa<DH, 2, 4>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    case 4: return launch_gqa<DH, 4, 2>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    case 7: return launch_gqa<DH, 7, 1>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    case 8: return launch_gqa<DH, 8, 1>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
     default: break;
   }
   // MHA and other ratios. With at least two 64-row blocks per CU (256 CUs)
@@ -670,10 +665,10 @@ static hipError_t attention_dh(const StepPlan& p, const bf16* q, const bf16* kc,
     tiles64 += (p.r[r].nrows + 63) / 64;
   }
   if (hq == hkv && max_rows > 32 && (long)hq * tiles64 >= 512)
-    return launch_gqa<DH, 1, 4, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+    return launch_gqa<DH, 1, 4>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
   return max_rows <= 32
-             ? launch_attn<DH, 2, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
-             : launch_attn<DH, 4, 2, kPLo>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
+             ? launch_attn<DH, 2, 2>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st)
+             : launch_attn<DH, 4, 2>(p, q, kc, vc, s_max, hq, hkv, out, scale_log2, st);
 }
 
 template <>

@@ -130,13 +130,15 @@ dlm_status dlm_ctl_update_threshold(const dlm_ctl_params* p, const dlm_ctl_insta
   if (s != DLM_OK) return s;
   const uint32_t all = p->n_gamma == 32 ? 0xffffffffu : ((1u << p->n_gamma) - 1u);
   if ((req->allowed & all) == 0) return fail("request has no allowed threshold");
-  int chosen = -1;
-  for (int gi = p->n_gamma - 1; gi >= 0; --gi) {   // descending over the allowed ones
+  // the highest allowed candidate that fits the remaining budget, else the
+  // lowest allowed one
+  int fit = -1, lowest = -1;
+  for (int gi = 0; gi < p->n_gamma; ++gi) {
     if (!((req->allowed >> gi) & 1u)) continue;
-    chosen = gi;
-    if (time_left(*p, *inst, *req, gi) <= req->slo_left_s) break;
+    if (lowest < 0) lowest = gi;
+    if (time_left(*p, *inst, *req, gi) <= req->slo_left_s) fit = gi;
   }
-  req->gamma_idx = chosen;
+  req->gamma_idx = fit >= 0 ? fit : lowest;
   return DLM_OK;
 }
 
@@ -196,21 +198,24 @@ dlm_status dlm_ctl_update_allowed(const dlm_ctl_params* p, dlm_ctl_req* reqs, in
     if (s != DLM_OK) return s;
   }
   if (std::isnan(capacity)) return fail("capacity is NaN");
-  // load of every later request at the lowest candidate
-  std::vector<double> min_remain(n > 0 ? n : 1, 0.0);
-  for (int i = n - 2; i >= 0; --i) min_remain[i] = min_remain[i + 1] + load(*p, reqs[i + 1], 0);
-  double used = 0.0;
+  // Worst case for request i: every earlier request at the maximum it was
+  // given (`given`), request i at a candidate, every later request at the
+  // lowest candidate. later[i] is that last sum; request i's maximum is the
+  // largest candidate that keeps the worst case within capacity (the lowest
+  // candidate when none does), and its allowed set every candidate up to it.
+  std::vector<double> later(n > 0 ? n : 1, 0.0);
+  double acc = 0.0;
+  for (int i = n - 1; i >= 0; --i) {
+    later[i] = acc;
+    acc += load(*p, reqs[i], 0);
+  }
+  double given = 0.0;
   for (int i = 0; i < n; ++i) {
-    uint32_t allowed = p->n_gamma == 32 ? 0xffffffffu : ((1u << p->n_gamma) - 1u);
-    for (int gi = p->n_gamma - 1; gi >= 0; --gi) {
-      const double l = load(*p, reqs[i], gi);
-      if (used + l + min_remain[i] <= capacity || gi == 0) {
-        used += l;
-        break;
-      }
-      allowed &= ~(1u << gi);
-    }
-    reqs[i].allowed = allowed;
+    int top = 0;
+    for (int gi = 1; gi < p->n_gamma; ++gi)
+      if (given + load(*p, reqs[i], gi) + later[i] <= capacity) top = gi;
+    given += load(*p, reqs[i], top);
+    reqs[i].allowed = top == 31 ? 0xffffffffu : ((2u << top) - 1u);
   }
   return DLM_OK;
 }

@@ -129,3 +129,50 @@ def test_alg1_monotone_in_budget():
             g = oc.update_conf_threshold(p, inst, r)
             assert g >= prev
             prev = g
+
+
+def test_alg2_brute_force_lexicographic_maximum():
+    """Load control against an exhaustive search on tiny batches with integer
+    loads (exact sums): the maxima given in arrival order are the
+    lexicographically largest assignment in which every request above the
+    lowest threshold has a worst case (earlier requests at their maxima, this
+    one at its maximum, later ones at the lowest threshold) within capacity."""
+    import itertools
+    for trial in range(400):
+        G, n = int(rng.integers(1, 4)), int(rng.integers(1, 5))
+        p = oc.Params(list(np.linspace(0.5, 0.9, G)))
+        reqs = [oc.Req(float(rng.integers(1, 20)),
+                       [float(x) for x in np.sort(rng.integers(1, 10, G))]) for _ in range(n)]
+        L = [[r.num_tokens * r.pred_steps_left[g] for g in range(G)] for r in reqs]
+        cap = float(rng.integers(0, int(sum(max(l) for l in L)) + 10))
+
+        def feasible(a):
+            for i in range(n):
+                worst = sum(L[j][a[j]] for j in range(i + 1)) + sum(L[j][0] for j in range(i + 1, n))
+                if a[i] > 0 and worst > cap:
+                    return False
+            return True
+
+        best = max(a for a in itertools.product(range(G), repeat=n) if feasible(a))
+        oc.update_allowed(p, reqs, cap)
+        assert [max(r.allowed) for r in reqs] == list(best), (trial, L, cap)
+        assert all(r.allowed == list(range(max(r.allowed) + 1)) for r in reqs)
+
+
+def test_alg1_brute_force_over_candidates():
+    """The threshold choice against every allowed candidate: the chosen one
+    fits the budget and no higher allowed one does, or none fits and it is the
+    lowest allowed."""
+    p = oc.Params([0.5, 0.6, 0.7, 0.8, 0.9], cache_block=32, max_seqs_per_batch=8)
+    inst = oc.Instance(oc.Profile(oc.Curve([256, 4096], [0.01, 0.08]),
+                                  oc.Curve([32, 256], [0.004, 0.01])), 3000.0, 5)
+    for r in _random_reqs(200, 5):
+        r.recomp_steps_left = min(r.recomp_steps_left, r.pred_steps_left[0])
+        r.allowed = sorted(set(int(x) for x in rng.integers(0, 5, int(rng.integers(1, 6)))))
+        g = oc.update_conf_threshold(p, inst, r)
+        t = {a: oc.predicted_time_left(p, inst, r, a) for a in r.allowed}
+        fitting = [a for a in r.allowed if t[a] <= r.slo_left_s]
+        if fitting:
+            assert t[g] <= r.slo_left_s and all(a <= g for a in fitting)
+        else:
+            assert g == min(r.allowed)
