@@ -44,6 +44,12 @@ __device__ __forceinline__ float wave_max(float v) {
 __device__ __forceinline__ f32x4 mfma16_bf16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+// 32x32x16 bf16: lane l supplies A[row = l%32][k = 8*(l/32) .. +7] and
+// B[col = l%32][k = 8*(l/32) .. +7]; D[row = 8*(i/4) + 4*(l/32) + i%4][col = l%32] = acc[i].
+__device__ __forceinline__ f32x16 mfma32_bf16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ int mf32_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 // 16x16x4 fp32: lane l supplies A[row = l%16][k = l/16], B[col = l%16][k = l/16].
 __device__ __forceinline__ f32x4 mfma16_f32(float a, float b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);

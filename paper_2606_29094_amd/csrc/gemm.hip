@@ -134,6 +134,7 @@ template <class Epi>
 hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
                           int K, int splits, int group_m, const Epi& epi, hipStream_t st);
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads);
+int gemm_dl_mfma(int cfg);
 
 // Register-staged kernel: any K that is a multiple of 16 bytes, fp32 or bf16.
 template <typename T, class Epi>
@@ -190,6 +191,7 @@ struct RoundTable {
   bool unsplit_only;
   int n;
   float kt[15], us[15];
+  int min_kt = 0;          // used only for at least this many k-tiles per block
 };
 const RoundTable kRoundTables[] = {
     {6, 1, 1 << 30, false, 15,
@@ -212,6 +214,19 @@ const RoundTable kRoundTables[] = {
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
      {17.1f, 22.4f, 25.6f, 37.3f, 33.5f, 40.8f, 51.1f, 65.7f, 65.8f, 71.1f, 90.8f, 119.1f, 171.0f, 214.9f, 335.1f}},
     {10, 3, 64, false, 1, {64}, {75.0f}},
+    // 32x32x16 MFMA tiles: 256x128 with four 128x64-wave tiles, and 384x256
+    // with eight 96x128-wave tiles (two waves per SIMD). Their round times
+    // were measured against configurations 29 and 6 in the same runs (full
+    // rounds, weights streamed from HBM) and scaled by those configurations'
+    // tables above, so all tables share one measurement basis.
+    {62, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {17.3f, 20.0f, 24.6f, 35.1f, 33.5f, 40.8f, 50.3f, 61.1f, 61.9f, 79.5f, 87.3f, 110.3f, 158.0f, 211.6f, 330.7f}},
+    {65, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {37.4f, 46.5f, 57.2f, 79.0f, 73.6f, 88.7f, 118.5f, 131.5f, 126.5f, 156.3f, 204.0f, 238.4f, 360.9f, 430.0f, 679.5f},
+     148},   // measured ahead only with long K walks (the GQA down projection); the
+             // table overrates it at 56 k-tiles (4096-row output projection 145 vs 112 us)
 };
 
 double round_us(const RoundTable& t, double kt) {
@@ -225,7 +240,7 @@ double round_us(const RoundTable& t, double kt) {
 }
 }  // namespace
 
-GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
+GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu, bool allow_mf32) {
   GemmPlan best{-1, 1, 0};
   if (M <= 0 || N <= 0) return best;
   if (es != 2 || K % 64 != 0) {
@@ -242,10 +257,12 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
   double best_t = 1e30;
   for (const RoundTable& c : kRoundTables) {
     if (M > c.max_m) continue;
+    if (!allow_mf32 && gemm_dl_mfma(c.cfg) == 32) continue;
     int bm, bn, th;
     gemm_dl_tile(c.cfg, &bm, &bn, &th);
     for (int s = 1; s <= 8; s *= 2) {
       if (s > 1 && (c.unsplit_only || !splittable || (K / 64) % s != 0 || K / s < 512)) continue;
+      if (K / 64 / s < c.min_kt) continue;
       const long units = (long)ceil_div(M, bm) * ceil_div(N, bn) * s;
       const long slots = (long)num_cu * c.occ;
       const long full = units / slots;
@@ -265,7 +282,7 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
   int bm, bn, th;
   if (best.cfg >= 0 && gemm_dl_tile(best.cfg, &bm, &bn, &th) && ceil_div(M, bm) > 1 &&
       (double)N * K * es > 256e6)
-    best.group_m = 16;
+    best.group_m = 8;
   return best;
 }
 
@@ -276,8 +293,15 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu) {
 // pitches (the 3584-wide GQA head) with the 2-stage ones (three blocks per CU,
 // 5.8 TB/s).
 GemmPlan lm_head_plan(int es, int M, int V, int K, int num_cu) {
-  GemmPlan p = gemm_plan(es, M, V, K, false, num_cu);
+  GemmPlan p = gemm_plan(es, M, V, K, false, num_cu, false);   // the head's epilogue is 16x16
   if (p.cfg >= 0 && M <= 64) p = GemmPlan{((long)K * es) % 8192 == 0 ? 11 : 10, 1, 0};
+  // The head is planned for its largest row count and skips, on the device,
+  // the row tiles beyond the rows that need a prediction. The grouped order
+  // must then span every row tile in one group: with several groups, the
+  // XCDs that receive the later groups' ranges would only hold skipped tiles
+  // (half the XCDs idle with two groups).
+  int bm, bn, th;
+  if (p.group_m > 0 && gemm_dl_tile(p.cfg, &bm, &bn, &th)) p.group_m = ceil_div(M, bm);
   return p;
 }
 
@@ -308,6 +332,8 @@ template <typename T>
 hipError_t gemm_swiglu(const GemmPlan& p, const T* A, int lda, const T* W, int ldw, int M, int F,
                        int K, T* out, int ldo, hipStream_t st) {
   if (p.splits != 1) return hipErrorInvalidValue;
+  // 32x32 tiles interleave gate and up columns in groups of 32
+  if (p.cfg >= 0 && gemm_dl_mfma(p.cfg) == 32 && F % 32 != 0) return hipErrorInvalidValue;
   EpiSwiGLU<T> e{out, ldo, M, F};
   return launch<T>(p, A, lda, W, ldw, M, 2 * F, K, e, st);
 }

@@ -49,8 +49,27 @@ __device__ __forceinline__ void store2(bf16* o, float a, float b) {
 struct EpiStore {
   float* C; int ldc; long split_stride; int M, N;
   static constexpr bool kRotateK = false;
+  static constexpr bool kMf32 = true;
+  __host__ __device__ void set_mfma(int) {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
+  // 32x32 accumulators: lanes 0-31 hold 32 consecutive columns of a row
+  template <int FM, int FN>
+  __device__ void op32(f32x16 (&acc)[FM][FN], int m0, int n0, int lane, int split) const {
+    float* Cz = C + (long)split * split_stride;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = m0 + fm * 32 + mf32_row(i, lane);
+        if (m >= M) continue;
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          const int n = n0 + fn * 32 + (lane & 31);
+          if (n < N) Cz[(long)m * ldc + n] = acc[fm][fn][i];
+        }
+      }
+  }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int, int, int, int split) const {
@@ -73,6 +92,10 @@ struct EpiStore {
 struct EpiScaledStore {
   float* C; int ldc; int M, N; float scale;
   static constexpr bool kRotateK = false;
+  static constexpr bool kMf32 = false;
+  __host__ __device__ void set_mfma(int) {}
+  template <int FM, int FN>
+  __device__ void op32(f32x16 (&)[FM][FN], int, int, int, int) const {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
   template <int FM, int FN>
@@ -99,8 +122,38 @@ struct EpiScaledStore {
 struct EpiAdd {
   float* C; int ldc; int M, N;
   static constexpr bool kRotateK = false;
+  static constexpr bool kMf32 = true;
+  __host__ __device__ void set_mfma(int) {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
+  // 32x32 accumulators: per tile row group of 4 rows, the loads first
+  template <int FM, int FN>
+  __device__ void op32(f32x16 (&acc)[FM][FN], int m0, int n0, int lane, int) const {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i0 = 0; i0 < 16; i0 += 4) {
+        float cv[4][FN];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = m0 + fm * 32 + mf32_row(i0 + i, lane);
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn) {
+            const int n = n0 + fn * 32 + (lane & 31);
+            cv[i][fn] = m < M && n < N ? C[(long)m * ldc + n] : 0.f;
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = m0 + fm * 32 + mf32_row(i0 + i, lane);
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn) {
+            const int n = n0 + fn * 32 + (lane & 31);
+            if (m < M && n < N) C[(long)m * ldc + n] = cv[i][fn] + acc[fm][fn][i0 + i];
+          }
+        }
+      }
+  }
   template <int FM, int FN>
   __device__ void operator()(f32x4 (&acc)[FM][FN], int m0, int n0, int lane, int,
                              char*, int, int, int, int, int) const {
@@ -129,18 +182,41 @@ struct EpiAdd {
   }
 };
 
-// Gate/up interleave: output column block of 32 = 16 gate columns followed by
-// the 16 up columns of the same ffn indices. GEMM column n maps to ffn index
-// f = (n / 32) * 16 + n % 16, gate when (n / 16) is even.
+// Gate/up interleave: with w = 16 (16x16 MFMA tiles) or 32 (32x32 tiles), an
+// output column block of 2w = w gate columns followed by the w up columns of
+// the same ffn indices. GEMM column n maps to ffn index f = (n / 2w) w + n % w,
+// gate when (n / w) is even. The loader reads weight row b_row(n).
 template <typename T>
 struct EpiSwiGLU {
   T* out; int ldo; int M; int F;   // F = d_ffn; GEMM N = 2F
+  int wsh = 4;                     // log2 w
+  __host__ __device__ void set_mfma(int mf) { wsh = mf == 32 ? 5 : 4; }
   __device__ int b_row(int n) const {
-    int f = (n >> 5) * 16 + (n & 15);
-    return ((n >> 4) & 1) ? F + f : f;
+    const int f = ((n >> (wsh + 1)) << wsh) + (n & ((1 << wsh) - 1));
+    return ((n >> wsh) & 1) ? F + f : f;
   }
   __device__ bool skip_tile(int) const { return false; }
   static constexpr bool kRotateK = false;
+  static constexpr bool kMf32 = true;
+  // 32x32 accumulators: tiles fn (gate) and fn + 1 (up) hold the same ffn
+  // indices in the same lanes; lanes 0-31 store 32 consecutive outputs of a row
+  template <int FM, int FN>
+  __device__ void op32(f32x16 (&acc)[FM][FN], int m0, int n0, int lane, int) const {
+    static_assert(FN % 2 == 0, "gate/up pairs");
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = m0 + fm * 32 + mf32_row(i, lane);
+#pragma unroll
+        for (int fn = 0; fn < FN; fn += 2) {
+          const float g = acc[fm][fn][i], u = acc[fm][fn + 1][i];
+          const float y = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+          const int f = ((n0 + fn * 32) >> 6) * 32 + (lane & 31);
+          if (m < M && f < F) out[(long)m * ldo + f] = from_f32<T>(y);
+        }
+      }
+  }
   // silu(g) * u with silu(g) = g / (1 + exp(-g)) through the hardware
   // reciprocal (about 1 ulp; the result is rounded to the storage type).
   // Outputs go out in pairs of adjacent columns: for rows i and i + 1 of a
@@ -195,6 +271,10 @@ struct EpiLMHead {
   float* pm; float* ps; int* pi; int M; int V; float inv_tau; int ld;  // ld = rows stride
   const int* m_count;
   static constexpr bool kRotateK = true;   // weight streaming: rotate the K walk per column tile
+  static constexpr bool kMf32 = false;
+  __host__ __device__ void set_mfma(int) {}
+  template <int FM, int FN>
+  __device__ void op32(f32x16 (&)[FM][FN], int, int, int, int) const {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int m0) const { return m_count && m0 >= *m_count; }
   template <int FM, int FN>

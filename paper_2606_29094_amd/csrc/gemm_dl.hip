@@ -10,22 +10,25 @@
 // is re-read by every column tile and mostly served from cache; B streams from
 // HBM and needs the deeper prefetch); no registers hold tiles in flight. The
 // MFMA part and the epilogues are the same as the register-staged kernel.
+#include <type_traits>
+
 #include "common.h"
 #include "gemm_common.h"
 #include "kernels.h"
 
 namespace dlm {
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, class Epi>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, class Epi>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int k_per_split, int group_m, Epi epi) {
   static_assert(RB == 64 || RB == 128, "k-tile row bytes");
   static_assert(SA >= 2 && SA <= 3 && SB >= SA && SB <= 4, "A and B stages");
+  static_assert(MF == 16 || MF == 32, "MFMA tile");
   constexpr int DA = SA - 1, DB = SB - 1;  // prefetch distances (k-tiles ahead)
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
-  constexpr int FM = TM / 16, FN = TN / 16;
+  constexpr int FM = TM / MF, FN = TN / MF;
   constexpr int BK = RB / 2;              // bf16 per row per k-tile
   constexpr int CPR = RB / 16;            // 16-byte chunks per row
   constexpr int RPI = 1024 / RB;          // rows per 1 KB wave instruction
@@ -84,57 +87,146 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   const int krot = Epi::kRotateK && nkt > 0 ? tn % nkt : 0;
   auto ktile = [&](int kt) { const int k = kt + krot; return k >= nkt ? k - nkt : k; };
 
-  // LDS chunk slot of global chunk c in row r: c ^ swz(r); 8 consecutive rows
-  // (two per 128-byte bank line for 64-byte rows) map to distinct banks.
-  auto swz = [](int r) { return CPR == 8 ? (r & 7) : ((r >> 1) & 3); };
-  // source of this lane for each of its wave's instructions (fixed over k)
-  const bf16* srcA[PERW_A];
-  const bf16* srcB[PERW_B];
+  // LDS chunk slot of global chunk c in row r: c ^ swz(r). With 16x16x32
+  // fragments (16 consecutive rows of one chunk per 16 lanes) 8 consecutive
+  // rows map to distinct banks (two per 128-byte bank line for 64-byte rows);
+  // with 32x32x16 fragments (32 consecutive rows of one chunk per 32 lanes)
+  // the slot follows row / 2, which keeps those reads free of bank conflicts
+  // (row & 7 gives ~4 conflict cycles per read, measured with
+  // SQ_LDS_BANK_CONFLICT). Both are invariant under row offsets that are
+  // multiples of the fragment height.
+  auto swz = [](int r) {
+    return CPR == 8 ? (MF == 32 ? ((r >> 1) & 7) : (r & 7)) : ((r >> 1) & 3);
+  };
+  // source of this lane for each of its wave's instructions (fixed over k),
+  // as 32-bit element offsets from the matrix base (operands hold fewer than
+  // 2^31 elements; half the registers of 64-bit pointers)
+  uint32_t srcA[PERW_A];
+  uint32_t srcB[PERW_B];
 #pragma unroll
   for (int j = 0; j < PERW_A; ++j) {
     const int row = RPI * (wave * PERW_A + j) + lane / CPR;
     const int cc = (lane % CPR) ^ swz(row);
-    srcA[j] = A + (long)min(m0 + row, M - 1) * lda + kbeg + cc * 8;
+    srcA[j] = (uint32_t)min(m0 + row, M - 1) * (uint32_t)lda + kbeg + cc * 8;
   }
 #pragma unroll
   for (int j = 0; j < PERW_B; ++j) {
     const int row = RPI * (wave * PERW_B + j) + lane / CPR;
     const int cc = (lane % CPR) ^ swz(row);
-    srcB[j] = B + (long)epi.b_row(min(n0 + row, N - 1)) * ldb + kbeg + cc * 8;
+    srcB[j] = (uint32_t)epi.b_row(min(n0 + row, N - 1)) * (uint32_t)ldb + kbeg + cc * 8;
   }
   auto issue_a = [&](int stage, int kt) {
     char* dst = smem + stage * STAGE_A + wave * PERW_A * 1024;
+    const bf16* base = A + kt * BK;
 #pragma unroll
     for (int j = 0; j < PERW_A; ++j)
-      __builtin_amdgcn_global_load_lds((gptr_t)(srcA[j] + kt * BK), (lptr_t)(dst + j * 1024), 16,
+      __builtin_amdgcn_global_load_lds((gptr_t)(base + srcA[j]), (lptr_t)(dst + j * 1024), 16,
                                        0, 0);
   };
   auto issue_b = [&](int stage, int kt) {
     char* dst = smem_b + stage * STAGE_B + wave * PERW_B * 1024;
+    const bf16* base = B + kt * BK;
 #pragma unroll
     for (int j = 0; j < PERW_B; ++j)
-      __builtin_amdgcn_global_load_lds((gptr_t)(srcB[j] + kt * BK), (lptr_t)(dst + j * 1024), 16,
+      __builtin_amdgcn_global_load_lds((gptr_t)(base + srcB[j]), (lptr_t)(dst + j * 1024), 16,
                                        0, 0);
   };
 
-  f32x4 acc[FM][FN];
+  // accumulators: 16x16 tiles (4 values per lane) or 32x32 tiles (16 per lane)
+  typedef typename std::conditional<MF == 32, f32x16, f32x4>::type Acc;
+  Acc acc[FM][FN];
 #pragma unroll
   for (int a = 0; a < FM; ++a)
 #pragma unroll
-    for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < FN; ++b) acc[a][b] = Acc{};
 
-  // fragment offsets: row R = base + (lane & 15) with base a multiple of 16,
-  // chunk c = 4 g + lane / 16, stored at slot c ^ swz(R) = c ^ swz(lane & 15)
-  const int a_row = (wm * TM + (lane & 15)) * RB;
-  const int b_row = (wn * TN + (lane & 15)) * RB;
-  int co[KG];
+  // fragment offsets. 16x16x32: row R = base + (lane & 15) with base a
+  // multiple of 16, chunk c = 4 g + lane / 16 (g: 32-wide k group), stored at
+  // slot c ^ swz(R) = c ^ swz(lane & 15). 32x32x16: row R = base + (lane & 31)
+  // with base a multiple of 32, chunk c = 2 s + lane / 32 (s: 16-wide k step),
+  // slot c ^ swz(lane & 31).
+  constexpr int LR = MF == 32 ? 31 : 15;
+  constexpr int NCO = MF == 32 ? RB / 32 : KG;
+  const int a_row = (wm * TM + (lane & LR)) * RB;
+  const int b_row = (wn * TN + (lane & LR)) * RB;
+  int co[NCO];
 #pragma unroll
-  for (int g = 0; g < KG; ++g) co[g] = ((g * 4 + (lane >> 4)) ^ swz(lane & 15)) << 4;
+  for (int g = 0; g < NCO; ++g)
+    co[g] = (MF == 32 ? ((2 * g + (lane >> 5)) ^ swz(lane & 31))
+                      : ((g * 4 + (lane >> 4)) ^ swz(lane & 15))) << 4;
+
+  // 32x32x16 tiles: per 16-wide k step, FM A and FN B fragments (one 16-byte
+  // LDS read each) feed FM x FN MFMAs; the next step's fragments are read
+  // while the current step's MFMAs run (two register buffers)
+  auto compute32 = [&](int sa, int sb) {
+    if constexpr (MF == 32) {
+      const char* pa = smem + sa * STAGE_A + a_row;
+      const char* pb = smem_b + sb * STAGE_B + b_row;
+      constexpr int KS = RB / 32;
+      u32x4 af[2][FM], bq[2][FN];
+      auto rd = [&](int buf, int st) {
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          af[buf][fm] = *reinterpret_cast<const u32x4*>(pa + fm * 32 * RB + co[st]);
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+          bq[buf][fn] = *reinterpret_cast<const u32x4*>(pb + fn * 32 * RB + co[st]);
+      };
+      // two fragment buffers unless the accumulators leave too few registers
+      // for them (then each step reads, then multiplies)
+      constexpr bool kTwoBuf = FM * FN * 16 + 8 * (FM + FN) <= 224;
+      if constexpr (!kTwoBuf) {
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+          rd(0, st);
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int fn = 0; fn < FN; ++fn)
+              acc[fm][fn] = mfma32_bf16(__builtin_bit_cast(bf16x8, af[0][fm]),
+                                        __builtin_bit_cast(bf16x8, bq[0][fn]), acc[fm][fn]);
+        }
+        return;
+      }
+      rd(0, 0);
+#pragma unroll
+      for (int st = 0; st < KS; ++st) {
+        if (st + 1 < KS) rd((st + 1) & 1, st + 1);
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn)
+            acc[fm][fn] = mfma32_bf16(__builtin_bit_cast(bf16x8, af[st & 1][fm]),
+                                      __builtin_bit_cast(bf16x8, bq[st & 1][fn]), acc[fm][fn]);
+      }
+      // schedule (mask 0x100: LDS reads, 0x008: MFMA): the first step's reads,
+      // then each step's MFMAs with the next step's reads spread among them
+      // (left to itself the compiler reuses one fragment register and waits
+      // on every read)
+      constexpr int NR = FM + FN, NM = FM * FN;
+      __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+#pragma unroll
+      for (int st = 0; st < KS; ++st) {
+        if (st + 1 < KS) {
+#pragma unroll
+          for (int i = 0; i < NR; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, NM / NR, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, NM - (NM / NR) * NR, 0);
+        } else {
+          __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+        }
+      }
+    }
+  };
 
   auto compute = [&](int sa, int sb) {
     const char* pa = smem + sa * STAGE_A;
     const char* pb = smem_b + sb * STAGE_B;
-    if constexpr (KG == 2) {
+    if constexpr (MF == 32) {
+      (void)pa; (void)pb;
+    } else if constexpr (KG == 2) {
       // Both k groups' fragments, then the MFMAs of group 0 with the reads of
       // group 1 spread among them, then the MFMAs of group 1: the LDS latency
       // of group 1 hides behind group 0's MFMAs (left to itself the compiler
@@ -219,29 +311,48 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     __builtin_amdgcn_sched_barrier(0);
     if (kt + DA < nkt) issue_a((kt + DA) % SA, ktile(kt + DA));
     if (kt + DB < nkt) issue_b((kt + DB) % SB, ktile(kt + DB));
-    compute(kt % SA, kt % SB);
+    if constexpr (MF == 32) compute32(kt % SA, kt % SB);
+    else compute(kt % SA, kt % SB);
   }
   __syncthreads();
-  epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
+  if constexpr (MF == 32)
+    epi.op32(acc, m0 + wm * TM, n0 + wn * TN, lane, tz);
+  else
+    epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
 }
 
 // Tile configurations (BM, BN, waves M x N, activation stages, weight stages,
-// k-tile row bytes).
-#define DL_CONFIGS(X)               \
-  X(1, 128, 128, 2, 2, 2, 2, 128)   \
-  X(6, 256, 256, 2, 4, 2, 2, 128)   \
-  X(10, 64, 128, 2, 2, 2, 2, 128)   \
-  X(11, 64, 128, 2, 2, 2, 3, 128)   \
-  X(21, 256, 192, 4, 2, 2, 2, 128)  \
-  X(22, 128, 192, 2, 2, 2, 2, 128)  \
-  X(29, 256, 128, 4, 2, 2, 3, 128)  \
-  X(42, 128, 192, 2, 2, 2, 3, 128)  \
-  X(43, 256, 128, 4, 2, 2, 4, 128)
+// k-tile row bytes, MFMA tile 16x16x32 or 32x32x16).
+#define DL_CONFIGS(X)                   \
+  X(1, 128, 128, 2, 2, 2, 2, 128, 16)   \
+  X(6, 256, 256, 2, 4, 2, 2, 128, 16)   \
+  X(10, 64, 128, 2, 2, 2, 2, 128, 16)   \
+  X(11, 64, 128, 2, 2, 2, 3, 128, 16)   \
+  X(21, 256, 192, 4, 2, 2, 2, 128, 16)  \
+  X(22, 128, 192, 2, 2, 2, 2, 128, 16)  \
+  X(29, 256, 128, 4, 2, 2, 3, 128, 16)  \
+  X(42, 128, 192, 2, 2, 2, 3, 128, 16)  \
+  X(43, 256, 128, 4, 2, 2, 4, 128, 16)  \
+  X(60, 256, 256, 2, 2, 2, 2, 128, 32)  \
+  X(61, 256, 256, 2, 2, 2, 3, 128, 32)  \
+  X(62, 256, 128, 2, 2, 2, 2, 128, 32)  \
+  X(63, 256, 256, 2, 4, 2, 2, 128, 32)  \
+  X(65, 384, 256, 4, 2, 2, 2, 128, 32)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_) \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_) \
   case id: *bm = BM_; *bn = BN_; *threads = WM_ * WN_ * 64; return 1;
+    DL_CONFIGS(X)
+#undef X
+  }
+  return 0;
+}
+
+int gemm_dl_mfma(int cfg) {
+  switch (cfg) {
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_) \
+  case id: return MF_;
     DL_CONFIGS(X)
 #undef X
   }
@@ -253,15 +364,22 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
                           int K, int splits, int group_m, const Epi& epi, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (K % 64 != 0 || splits < 1 || (K / 64) % splits != 0) return hipErrorInvalidValue;
+  // the kernel addresses operands with 32-bit element offsets
+  if ((double)(M - 1) * lda + K >= 4294967296.0 || (double)(N - 1) * ldb + K >= 4294967296.0)
+    return hipErrorInvalidValue;
   const int kps = K / splits;
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_)                                            \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                                        \
   case id: {                                                                             \
-    dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                  \
-    DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, Epi>), g,        \
-                       dim3(WM_ * WN_ * 64),                                             \
-                       0, st, A, lda, B, ldb, M, N, K, kps, group_m, epi);                        \
-    return hipGetLastError();                                                            \
+    if constexpr (MF_ == 32 && !Epi::kMf32) return hipErrorInvalidValue;                 \
+    else {                                                                               \
+      dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                \
+      Epi e = epi;                                                                       \
+      e.set_mfma(MF_);                                                                   \
+      DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, Epi>), g,        \
+                 dim3(WM_ * WN_ * 64), 0, st, A, lda, B, ldb, M, N, K, kps, group_m, e);   \
+      return hipGetLastError();                                                          \
+    }                                                                                    \
   }
     DL_CONFIGS(X)
 #undef X

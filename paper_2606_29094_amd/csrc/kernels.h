@@ -50,7 +50,11 @@ __device__ __forceinline__ int plan_req_of_tile(const StepPlan& p, int tile) {
 // cfg >= 0: a direct-load tile configuration (bf16); cfg < 0: register-staged
 // kernel. splits: number of K slices (fp32 partial slices, summed by the consumer).
 struct GemmPlan { int cfg; int splits; int group_m; };   // group_m: tile order (0 = plain)
-GemmPlan gemm_plan(int elem_bytes, int M, int N, int K, bool splittable, int num_cu);
+// allow_mf32: configurations with 32x32x16 MFMA tiles may be chosen (their
+// epilogues exist for the plain, residual-add and SwiGLU stores; SwiGLU needs
+// d_ffn % 32 == 0)
+GemmPlan gemm_plan(int elem_bytes, int M, int N, int K, bool splittable, int num_cu,
+                   bool allow_mf32 = true);
 // plan of the LM-head GEMM (M rows x V vocab entries)
 GemmPlan lm_head_plan(int elem_bytes, int M, int V, int K, int num_cu);
 template <typename T>

@@ -194,7 +194,9 @@ Layout layout(const dlm_model* m, int n, int n_req) {
   const int es_i = (int)m->es;
   L.g_qkv = gemm_plan(es_i, n, qkv_dim, c.d_model, true, m->num_cu);
   L.g_o = gemm_plan(es_i, n, c.d_model, qd, true, m->num_cu);
-  L.g_gu = gemm_plan(es_i, n, 2 * c.d_ffn, c.d_model, false, m->num_cu);
+  // the SwiGLU GEMM keeps 16x16 tiles: its 32x32 variants measured 5-6 %
+  // slower on every gate/up shape
+  L.g_gu = gemm_plan(es_i, n, 2 * c.d_ffn, c.d_model, false, m->num_cu, false);
   L.g_down = gemm_plan(es_i, n, c.d_model, c.d_ffn, true, m->num_cu);
   L.m_max = std::min(n, n_req * kMaxBlock);
   L.g_lm = lm_head_plan(es_i, L.m_max, c.vocab, c.d_model, m->num_cu);
