@@ -3,13 +3,16 @@
 // Each k-tile is 64 bf16 (128 bytes) of BM rows of A and BN rows of B. A wave
 // instruction moves 8 rows (1 KB): lane l writes LDS bytes [16 l, 16 l + 16)
 // of that kilobyte, and it fetches the global 16-byte chunk that belongs
-// there under an XOR swizzle (LDS chunk slot = global chunk ^ (row & 7)), so
-// that the 16 lanes that later read 16 consecutive rows of one chunk hit
-// distinct banks. The weight operand B goes SB-1 k-tiles ahead through a ring of
-// SB LDS stages and the activation operand A one k-tile ahead through two (A
-// is re-read by every column tile and mostly served from cache; B streams from
-// HBM and needs the deeper prefetch); no registers hold tiles in flight. The
-// MFMA part and the epilogues are the same as the register-staged kernel.
+// there under an XOR swizzle (LDS chunk slot = global chunk ^ swz(row)), so
+// that the lanes that later read consecutive rows of one chunk hit distinct
+// banks. The weight operand B goes SB-1 k-tiles ahead through a ring of SB LDS
+// stages and the activation operand A one k-tile ahead through two (A is
+// re-read by every column tile and mostly served from cache; B streams from
+// HBM and needs the deeper prefetch); no registers hold tiles in flight.
+// Waves multiply with v_mfma_f32_16x16x32_bf16 (MF = 16) or
+// v_mfma_f32_32x32x16_bf16 (MF = 32); the 16x16 epilogues are the same as the
+// register-staged kernel's, the 32x32 ones (plain, residual-add and SwiGLU
+// stores) follow the 32x32 accumulator layout.
 #include <type_traits>
 
 #include "common.h"
@@ -333,10 +336,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   X(29, 256, 128, 4, 2, 2, 3, 128, 16)  \
   X(42, 128, 192, 2, 2, 2, 3, 128, 16)  \
   X(43, 256, 128, 4, 2, 2, 4, 128, 16)  \
-  X(60, 256, 256, 2, 2, 2, 2, 128, 32)  \
-  X(61, 256, 256, 2, 2, 2, 3, 128, 32)  \
   X(62, 256, 128, 2, 2, 2, 2, 128, 32)  \
-  X(63, 256, 256, 2, 4, 2, 2, 128, 32)  \
   X(65, 384, 256, 4, 2, 2, 2, 128, 32)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
