@@ -50,6 +50,7 @@ struct EpiStore {
   float* C; int ldc; long split_stride; int M, N;
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = true;
+  static constexpr bool kTailSplit = true;   // last-round tiles may be split
   __host__ __device__ void set_mfma(int) {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
@@ -93,6 +94,7 @@ struct EpiScaledStore {
   float* C; int ldc; int M, N; float scale;
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = false;
+  static constexpr bool kTailSplit = false;   // last-round tiles may be split
   __host__ __device__ void set_mfma(int) {}
   template <int FM, int FN>
   __device__ void op32(f32x16 (&)[FM][FN], int, int, int, int) const {}
@@ -123,6 +125,7 @@ struct EpiAdd {
   float* C; int ldc; int M, N;
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = true;
+  static constexpr bool kTailSplit = true;   // last-round tiles may be split
   __host__ __device__ void set_mfma(int) {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
@@ -198,6 +201,7 @@ struct EpiSwiGLU {
   __device__ bool skip_tile(int) const { return false; }
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = true;
+  static constexpr bool kTailSplit = true;   // last-round tiles may be split
   // 32x32 accumulators: tiles fn (gate) and fn + 1 (up) hold the same ffn
   // indices in the same lanes; lanes 0-31 store 32 consecutive outputs of a row
   template <int FM, int FN>
@@ -272,6 +276,7 @@ struct EpiLMHead {
   const int* m_count;
   static constexpr bool kRotateK = true;   // weight streaming: rotate the K walk per column tile
   static constexpr bool kMf32 = false;
+  static constexpr bool kTailSplit = false;   // last-round tiles may be split
   __host__ __device__ void set_mfma(int) {}
   template <int FM, int FN>
   __device__ void op32(f32x16 (&)[FM][FN], int, int, int, int) const {}

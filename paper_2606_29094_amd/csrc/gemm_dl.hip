@@ -21,10 +21,14 @@
 
 namespace dlm {
 
+// One BM x BN output tile at rows m0.., columns n0.., K range [kbeg, kend),
+// with the block's LDS at smem. tn and tz (column tile, K slice) are passed
+// to the K order and the epilogue.
 template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, class Epi>
-__global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
-    const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
-    int K, int k_per_split, int group_m, Epi epi) {
+__device__ __forceinline__ void dl_tile(char* smem, const bf16* __restrict__ A, int lda,
+                                        const bf16* __restrict__ B, int ldb, int M, int N,
+                                        int m0, int n0, int tn, int tz, int kbeg, int kend,
+                                        const Epi& epi) {
   static_assert(RB == 64 || RB == 128, "k-tile row bytes");
   static_assert(SA >= 2 && SA <= 3 && SB >= SA && SB <= 4, "A and B stages");
   static_assert(MF == 16 || MF == 32, "MFMA tile");
@@ -32,6 +36,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   constexpr int FM = TM / MF, FN = TN / MF;
+  static_assert(FM * MF == TM && FN * MF == TN, "wave tile");
   constexpr int BK = RB / 2;              // bf16 per row per k-tile
   constexpr int CPR = RB / 16;            // 16-byte chunks per row
   constexpr int RPI = 1024 / RB;          // rows per 1 KB wave instruction
@@ -43,43 +48,10 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   // issued after A(kt) in the steady issue order (see the pipeline below)
   constexpr int INFLIGHT = DB > DA ? DA * PERW_B + (DA - 1) * PERW_A : (DA - 1) * (PERW_A + PERW_B);
   static_assert(INFLIGHT < 64, "vmcnt range");
-  __shared__ __attribute__((aligned(1024))) char smem[SA * STAGE_A + SB * STAGE_B];
   char* const smem_b = smem + SA * STAGE_A;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  // Tile order. group_m == 0: block (x, y, z) = (column tile, row tile,
-  // K slice). group_m > 0 (weight matrices larger than the last-level cache):
-  // the dispatcher hands out blocks in linear order (x fastest, then y, then
-  // z) round-robin over the 8 XCDs (block i to XCD i mod 8), each with its
-  // own L2. The linear id is remapped so that each XCD receives one contiguous
-  // range of a logical order that goes down a group of group_m row tiles
-  // before moving to the next column tile: blocks sharing a weight column
-  // tile run on the same XCD at about the same time, and each column tile is
-  // fetched from HBM about once per group of row tiles instead of once per
-  // row tile.
-  int tm = blockIdx.y, tn = blockIdx.x, tz = blockIdx.z;
-  if (group_m > 0) {
-    const int n_n = gridDim.x, n_m = gridDim.y;
-    const int plane = n_n * n_m;
-    const int total = plane * gridDim.z;
-    const int id = (blockIdx.z * n_m + blockIdx.y) * n_n + blockIdx.x;
-    const int xcd = id % kXcds, per = total / kXcds, rem = total % kXcds;
-    const int lid = xcd * per + min(xcd, rem) + id / kXcds;
-    tz = lid / plane;
-    const int l = lid - tz * plane;
-    const int per_group = group_m * n_n;
-    const int gi = l / per_group;
-    const int first = gi * group_m;
-    const int gsz = min(n_m - first, group_m);
-    const int r = l - gi * per_group;
-    tm = first + r % gsz;
-    tn = r / gsz;
-  }
-  const int m0 = tm * BM, n0 = tn * BN;
-  if (epi.skip_tile(m0)) return;   // uniform over the block
-  const int kbeg = tz * k_per_split;
-  const int kend = min(K, kbeg + k_per_split);
   const int nkt = kend > kbeg ? (kend - kbeg) / BK : 0;
   // K order: epilogues that ask for it (the LM head, which streams a large
   // weight matrix with a 2^n-byte row pitch) start each column tile's K walk
@@ -324,6 +296,115 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
 }
 
+// Sub-tiles of the last round: tile shapes a BM x BN tile splits into with the
+// same waves (halves: two (BM/2) x BN tiles; quarters: four (BM/2) x (BN/2)).
+template <int BM, int BN, int WAVES_M, int WAVES_N, int RB, int MF>
+struct SubTiles {
+  static constexpr int NW = WAVES_M * WAVES_N, RPI = 1024 / RB;
+  static constexpr bool fits(int bm, int bn) {
+    return bm % (RPI * NW) == 0 && bn % (RPI * NW) == 0 && (bm / WAVES_M) % MF == 0 &&
+           (bn / WAVES_N) % (2 * MF) == 0;
+  }
+  static constexpr bool kHalf = fits(BM / 2, BN);
+  static constexpr bool kQuarter = fits(BM / 2, BN / 2);
+};
+
+// Grid: one block per tile of the logical order (a 3-D grid of column tiles x
+// row tiles x K slices), except that the last n_tail tiles of that order may
+// each be split into `sub` (2 or 4) sub-tiles, one block each, launched after
+// all whole tiles (then a 1-D grid): when the tile count leaves a last round
+// that fills at most half of the CUs, its tiles then finish in a fraction of a
+// whole tile's time. Sub-tiles accumulate every output element over the same
+// k order as whole tiles, so the results are the same bit for bit.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, bool TAIL,
+          class Epi>
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
+    int K, int k_per_split, int n_n, int n_m, int group_m, int n_tail, int sub, Epi epi) {
+  __shared__ __attribute__((aligned(1024))) char smem[(SA * BM + SB * BN) * RB];
+  // Tile order. The logical order enumerates (K slice, row tile, column tile)
+  // with the column tile fastest (group_m == 0), or, for weight matrices
+  // larger than the last-level cache (group_m > 0), goes down a group of
+  // group_m row tiles before moving to the next column tile, so that each
+  // weight column tile is fetched from HBM about once per group of row tiles
+  // instead of once per row tile. The dispatcher hands out blocks in linear
+  // order round-robin over the 8 XCDs (block i to XCD i mod 8), each with its
+  // own L2; with group_m > 0 the whole tiles are remapped so that each XCD
+  // receives one contiguous range of the logical order (blocks sharing a
+  // weight column tile run on the same XCD at about the same time).
+  // (TAIL: the instance for launches with sub-tiles, a 1-D grid; the other
+  // one has whole tiles only and a 3-D grid)
+  // logical tile lid -> (K slice, row tile, column tile)
+  auto logical = [&](int lid, int& tz, int& tm, int& tn) {
+    const int plane = n_n * n_m;
+    tz = lid / plane;
+    const int l = lid - tz * plane;
+    if (group_m > 0) {
+      const int per_group = group_m * n_n;
+      const int gi = l / per_group;
+      const int first = gi * group_m;
+      const int gsz = min(n_m - first, group_m);
+      const int r = l - gi * per_group;
+      tm = first + r % gsz;
+      tn = r / gsz;
+    } else {
+      tm = l / n_n;
+      tn = l - tm * n_n;
+    }
+  };
+  // linear dispatch id -> logical tile: each XCD a contiguous range of nb tiles
+  auto xcd_range = [](int id, int nb) {
+    const int xcd = id % kXcds, per = nb / kXcds, rem = nb % kXcds;
+    return xcd * per + min(xcd, rem) + id / kXcds;
+  };
+  int tz, tm, tn, part = 0;
+  bool is_sub = false;
+  if constexpr (!TAIL) {
+    tm = blockIdx.y;
+    tn = blockIdx.x;
+    tz = blockIdx.z;
+    if (group_m > 0) {
+      const int id = (blockIdx.z * n_m + blockIdx.y) * n_n + blockIdx.x;
+      logical(xcd_range(id, n_n * n_m * (int)gridDim.z), tz, tm, tn);
+    }
+  } else {
+    const int n_main = n_n * n_m * (K / k_per_split) - n_tail;
+    const int id = blockIdx.x;
+    if (id < n_main) {
+      logical(group_m > 0 ? xcd_range(id, n_main) : id, tz, tm, tn);
+    } else {
+      is_sub = true;
+      part = (id - n_main) % sub;
+      logical(n_main + (id - n_main) / sub, tz, tm, tn);
+    }
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
+  if (epi.skip_tile(m0)) return;   // uniform over the block
+  const int kbeg = tz * k_per_split;
+  const int kend = min(K, kbeg + k_per_split);
+  typedef SubTiles<BM, BN, WAVES_M, WAVES_N, RB, MF> Sub;
+  if (is_sub) {
+    if constexpr (TAIL && Epi::kTailSplit && Sub::kQuarter) {
+      if (sub == 4) {
+        dl_tile<BM / 2, BN / 2, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
+            smem, A, lda, B, ldb, M, N, m0 + (part >> 1) * (BM / 2), n0 + (part & 1) * (BN / 2),
+            tn, tz, kbeg, kend, epi);
+        return;
+      }
+    }
+    if constexpr (TAIL && Epi::kTailSplit && Sub::kHalf) {
+      if (sub == 2) {
+        dl_tile<BM / 2, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
+            smem, A, lda, B, ldb, M, N, m0 + part * (BM / 2), n0, tn, tz, kbeg, kend, epi);
+        return;
+      }
+    }
+    return;   // not reached: the launcher only splits where the shapes allow
+  }
+  dl_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn,
+                                                          tz, kbeg, kend, epi);
+}
+
 // Tile configurations (BM, BN, waves M x N, activation stages, weight stages,
 // k-tile row bytes, MFMA tile 16x16x32 or 32x32x16).
 #define DL_CONFIGS(X)                   \
@@ -359,25 +440,55 @@ int gemm_dl_mfma(int cfg) {
   return 0;
 }
 
+// Sub-tile splits a configuration allows for the last round (bit 1: halves,
+// bit 2: quarters).
+int gemm_dl_subs(int cfg) {
+  switch (cfg) {
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                          \
+  case id: {                                                                \
+    typedef SubTiles<BM_, BN_, WM_, WN_, RB_, MF_> S;                       \
+    return (S::kHalf ? 2 : 0) | (S::kQuarter ? 4 : 0);                      \
+  }
+    DL_CONFIGS(X)
+#undef X
+  }
+  return 0;
+}
+
 template <class Epi>
 hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
-                          int K, int splits, int group_m, const Epi& epi, hipStream_t st) {
+                          int K, int splits, int group_m, int sub, int n_tail, const Epi& epi,
+                          hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (K % 64 != 0 || splits < 1 || (K / 64) % splits != 0) return hipErrorInvalidValue;
   // the kernel addresses operands with 32-bit element offsets
   if ((double)(M - 1) * lda + K >= 4294967296.0 || (double)(N - 1) * ldb + K >= 4294967296.0)
     return hipErrorInvalidValue;
   const int kps = K / splits;
+  if (sub == 0) n_tail = 0;
+  if (n_tail < 0 || (sub != 0 && (!Epi::kTailSplit || !(gemm_dl_subs(cfg) & sub))))
+    return hipErrorInvalidValue;
   switch (cfg) {
 #define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                                        \
   case id: {                                                                             \
     if constexpr (MF_ == 32 && !Epi::kMf32) return hipErrorInvalidValue;                 \
     else {                                                                               \
-      dim3 g(ceil_div(N, BN_), ceil_div(M, BM_), splits);                                \
+      const int n_n = ceil_div(N, BN_), n_m = ceil_div(M, BM_);                          \
+      const long total = (long)n_n * n_m * splits;                                       \
+      if (n_tail > total) return hipErrorInvalidValue;                                   \
+      const long blocks = total - n_tail + (long)sub * n_tail;                           \
+      if (blocks >= (1L << 31)) return hipErrorInvalidValue;                             \
       Epi e = epi;                                                                       \
       e.set_mfma(MF_);                                                                   \
-      DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, Epi>), g,        \
-                 dim3(WM_ * WN_ * 64), 0, st, A, lda, B, ldb, M, N, K, kps, group_m, e);   \
+      if (n_tail == 0) {                                                                 \
+        DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, false, Epi>),   \
+                   dim3(n_n, n_m, splits), dim3(WM_ * WN_ * 64), 0, st, A, lda, B, ldb, M, \
+                   N, K, kps, n_n, n_m, group_m, 0, 0, e);                               \
+      } else if constexpr (Epi::kTailSplit) {                                            \
+        DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, true, Epi>),    \
+                   dim3((unsigned)blocks), dim3(WM_ * WN_ * 64), 0, st, A, lda, B, ldb, M, \
+                   N, K, kps, n_n, n_m, group_m, n_tail, sub, e);                        \
+      }                                                                                  \
       return hipGetLastError();                                                          \
     }                                                                                    \
   }
@@ -388,16 +499,14 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
 }
 
 template hipError_t gemm_dl_launch<EpiStore>(int, const bf16*, int, const bf16*, int, int, int,
-                                             int, int, int, const EpiStore&, hipStream_t);
+    int, int, int, int, int, const EpiStore&, hipStream_t);
 template hipError_t gemm_dl_launch<EpiAdd>(int, const bf16*, int, const bf16*, int, int, int,
-                                           int, int, int, const EpiAdd&, hipStream_t);
-template hipError_t gemm_dl_launch<EpiScaledStore>(int, const bf16*, int, const bf16*, int, int,
-                                                   int, int, int, int, const EpiScaledStore&,
-                                                   hipStream_t);
-template hipError_t gemm_dl_launch<EpiSwiGLU<bf16>>(int, const bf16*, int, const bf16*, int, int,
-                                                    int, int, int, int, const EpiSwiGLU<bf16>&,
-                                                    hipStream_t);
+    int, int, int, int, int, const EpiAdd&, hipStream_t);
+template hipError_t gemm_dl_launch<EpiScaledStore>(int, const bf16*, int, const bf16*, int, int, int,
+    int, int, int, int, int, const EpiScaledStore&, hipStream_t);
+template hipError_t gemm_dl_launch<EpiSwiGLU<bf16>>(int, const bf16*, int, const bf16*, int, int, int,
+    int, int, int, int, int, const EpiSwiGLU<bf16>&, hipStream_t);
 template hipError_t gemm_dl_launch<EpiLMHead>(int, const bf16*, int, const bf16*, int, int, int,
-                                              int, int, int, const EpiLMHead&, hipStream_t);
+    int, int, int, int, int, const EpiLMHead&, hipStream_t);
 
 }  // namespace dlm

@@ -49,12 +49,29 @@ __device__ __forceinline__ int plan_req_of_tile(const StepPlan& p, int tile) {
 // ---- GEMM family (gemm.hip, gemm_dl.hip) ----
 // cfg >= 0: a direct-load tile configuration (bf16); cfg < 0: register-staged
 // kernel. splits: number of K slices (fp32 partial slices, summed by the consumer).
-struct GemmPlan { int cfg; int splits; int group_m; };   // group_m: tile order (0 = plain)
+// group_m: tile order (0 = plain); sub, n_tail: the last n_tail tiles of the
+// order are each run as `sub` (2 or 4) sub-tiles (0: none)
+struct GemmPlan { int cfg; int splits; int group_m; int sub = 0; int n_tail = 0; };
 // allow_mf32: configurations with 32x32x16 MFMA tiles may be chosen (their
 // epilogues exist for the plain, residual-add and SwiGLU stores; SwiGLU needs
 // d_ffn % 32 == 0)
+// direct-load bf16 kernel: one launch of configuration cfg; its output tile,
+// MFMA shape and the sub-tile splits it allows (bit 1: halves, bit 2: quarters)
+template <class Epi>
+hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
+                          int K, int splits, int group_m, int sub, int n_tail, const Epi& epi,
+                          hipStream_t st);
+int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads);
+int gemm_dl_mfma(int cfg);
+int gemm_dl_subs(int cfg);
+// one launch of configuration cfg with epilogue 0 (fp32 store), 1 (SwiGLU to
+// bf16, N = 2 F) or 2 (fp32 add), A [M, K], B [N, K], C row-major (test hook)
+hipError_t gemm_debug_launch(int cfg, int epilogue, int sub, int n_tail, int group_m,
+                             const bf16* A, const bf16* B, void* C, int M, int N, int K,
+                             hipStream_t st);
+// allow_tail: the last round may be split into sub-tiles (epilogues that allow it)
 GemmPlan gemm_plan(int elem_bytes, int M, int N, int K, bool splittable, int num_cu,
-                   bool allow_mf32 = true);
+                   bool allow_mf32 = true, bool allow_tail = true);
 // plan of the LM-head GEMM (M rows x V vocab entries)
 GemmPlan lm_head_plan(int elem_bytes, int M, int V, int K, int num_cu);
 template <typename T>

@@ -805,4 +805,44 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
   return DLM_OK;
 }
 
+dlm_status dlm_debug_gemm_info(int32_t cfg, int32_t* bm, int32_t* bn, int32_t* subs) {
+  g_err.clear();
+  int tm = 0, tn = 0, th = 0;
+  if (!gemm_dl_tile(cfg, &tm, &tn, &th)) return fail(DLM_EINVAL, "no GEMM configuration %d", cfg);
+  if (bm) *bm = tm;
+  if (bn) *bn = tn;
+  if (subs) *subs = gemm_dl_subs(cfg);
+  return DLM_OK;
+}
+
+dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_tail,
+                          int32_t group_m, const void* a, const void* b, void* c, int32_t M,
+                          int32_t N, int32_t K, void* stream) {
+  g_err.clear();
+  if (!a || !b || !c) return fail(DLM_EINVAL, "NULL buffer");
+  if (M < 1 || N < 1 || K < 1 || K % 64 != 0)
+    return fail(DLM_EINVAL, "sizes M %d N %d K %d (K a positive multiple of 64)", M, N, K);
+  if (epilogue < 0 || epilogue > 2) return fail(DLM_EINVAL, "epilogue %d", epilogue);
+  if (epilogue == 1 && N % 2 != 0) return fail(DLM_EINVAL, "odd N %d for the SwiGLU epilogue", N);
+  if (group_m < 0 || n_tail < 0) return fail(DLM_EINVAL, "negative group_m or n_tail");
+  int tm = 0, tn = 0, th = 0;
+  if (!gemm_dl_tile(cfg, &tm, &tn, &th)) return fail(DLM_EINVAL, "no GEMM configuration %d", cfg);
+  // the gate/up interleave pairs columns in groups of the MFMA tile width
+  const int pair = gemm_dl_mfma(cfg) == 32 ? 32 : 16;
+  if (epilogue == 1 && (N / 2) % pair != 0)
+    return fail(DLM_EINVAL, "SwiGLU width %d is not a multiple of %d", N / 2, pair);
+  if (sub != 0 && ((sub != 2 && sub != 4) || !(gemm_dl_subs(cfg) & sub)))
+    return fail(DLM_EINVAL, "configuration %d has no %d-way sub-tiles", cfg, sub);
+  if (sub != 0 && (long)n_tail > (long)ceil_div(M, tm) * ceil_div(N, tn))
+    return fail(DLM_EINVAL, "n_tail %d beyond the tile count", n_tail);
+  const hipError_t e = gemm_debug_launch(cfg, epilogue, sub, n_tail, group_m,
+                                         reinterpret_cast<const bf16*>(a),
+                                         reinterpret_cast<const bf16*>(b), c, M, N, K,
+                                         reinterpret_cast<hipStream_t>(stream));
+  if (e == hipErrorInvalidValue)
+    return fail(DLM_EINVAL, "GEMM configuration %d rejects this launch", cfg);
+  if (e != hipSuccess) return fail(DLM_EHIP, "GEMM launch: %s", hipGetErrorString(e));
+  return DLM_OK;
+}
+
 }  // extern "C"

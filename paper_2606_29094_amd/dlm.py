@@ -26,7 +26,7 @@ MODES = {"none": DLM_CACHE_NONE, "prefix": DLM_CACHE_PREFIX, "dual": DLM_CACHE_D
 EXPORTS = ["dlm_load_weights", "dlm_model_destroy", "dlm_workspace_bytes",
            "dlm_kv_cache_alloc", "dlm_cache_destroy", "dlm_cache_invalidate",
            "dlm_denoise_step", "dlm_denoise_step_noalloc", "dlm_cache_refresh",
-           "dlm_debug_logits", "dlm_debug_trace",
+           "dlm_debug_logits", "dlm_debug_trace", "dlm_debug_gemm_info", "dlm_debug_gemm",
            "dlm_head_confidence", "dlm_profile_enable", "dlm_profile_read",
            "dlm_profile_sample", "dlm_ceiling_mfma", "dlm_ceiling_copy", "dlm_last_error"]
 
@@ -119,6 +119,10 @@ def lib():
                                       c_void_p, c_size_t, c_void_p]
         L.dlm_head_confidence.argtypes = [c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
                                           c_void_p, c_size_t, c_void_p]
+        L.dlm_debug_gemm_info.argtypes = [c_int32, POINTER(c_int32), POINTER(c_int32),
+                                          POINTER(c_int32)]
+        L.dlm_debug_gemm.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p,
+                                     c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p]
         L.dlm_profile_enable.argtypes = [c_void_p, c_int32, ctypes.c_char_p]
         L.dlm_profile_read.argtypes = [c_void_p, POINTER(DlmProfileEntry), c_int32,
                                        POINTER(c_int32)]
@@ -132,6 +136,7 @@ def lib():
                      "dlm_cache_invalidate", "dlm_denoise_step", "dlm_denoise_step_noalloc",
                      "dlm_cache_refresh",
                      "dlm_debug_logits", "dlm_debug_trace", "dlm_head_confidence",
+                     "dlm_debug_gemm_info", "dlm_debug_gemm",
                      "dlm_profile_enable",
                      "dlm_profile_read", "dlm_profile_sample"]:
             getattr(L, name).restype = c_int32
@@ -256,6 +261,34 @@ def head_confidence(model, u_rows, m_rows: int, conf, tok, workspace, stream=Non
                                     _ptr(workspace),
                                     workspace.numel() * workspace.element_size(),
                                     _stream(stream)))
+
+
+def debug_gemm_info(cfg: int):
+    """(bm, bn, allowed sub-tile splits bitmask) of a GEMM tile configuration,
+    or None when the configuration does not exist."""
+    bm, bn, subs = c_int32(), c_int32(), c_int32()
+    rc = lib().dlm_debug_gemm_info(cfg, ctypes.byref(bm), ctypes.byref(bn), ctypes.byref(subs))
+    if rc != DLM_OK:
+        return None
+    return bm.value, bn.value, subs.value
+
+
+def debug_gemm(cfg: int, epilogue: int, a, b, c, sub: int = 0, n_tail: int = 0,
+               group_m: int = 0, stream=None):
+    """One launch of GEMM configuration cfg: epilogue 0 stores a @ b.T (fp32),
+    1 stores silu(gate) * up (bf16, N/2 columns), 2 adds a @ b.T into c."""
+    M, K = a.shape
+    N = b.shape[0]
+    for t in (a, b, c):
+        if not t.is_contiguous():
+            raise ValueError("GEMM operands must be contiguous")
+    if b.shape[1] != K:
+        raise ValueError("a and b disagree on K")
+    want = (M, N // 2) if epilogue == 1 else (M, N)
+    if tuple(c.shape) != want:
+        raise ValueError(f"c has shape {tuple(c.shape)}, expected {want}")
+    check(lib().dlm_debug_gemm(cfg, epilogue, sub, n_tail, group_m, _ptr(a), _ptr(b), _ptr(c),
+                               M, N, K, _stream(stream)))
 
 
 def profile_enable(model, on: bool, only_class: str | None = None):

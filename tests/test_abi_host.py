@@ -241,3 +241,31 @@ def test_profile_sample_validation():
         dlm.model_destroy(m)
     with pytest.raises(dlm.DlmError):
         dlm.profile_sample(None, 2)
+
+
+def test_debug_gemm_validation_on_host():
+    """Tile-configuration queries and the GEMM hook's argument checks run on
+    the host: malformed launches are rejected before anything is enqueued."""
+    L = _lib_or_skip()
+    bm, bn, subs = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    assert L.dlm_debug_gemm_info(6, ctypes.byref(bm), ctypes.byref(bn), ctypes.byref(subs)) == 0
+    assert (bm.value, bn.value, subs.value) == (256, 256, 6)      # halves and quarters
+    assert L.dlm_debug_gemm_info(65, ctypes.byref(bm), ctypes.byref(bn), ctypes.byref(subs)) == 0
+    assert (bm.value, bn.value, subs.value) == (384, 256, 0)
+    assert L.dlm_debug_gemm_info(999, None, None, None) == dlm.DLM_EINVAL
+    F = FAKE
+
+    def call(cfg=6, epi=0, sub=0, tail=0, group=0, a=F, b=F, c=F, M=300, N=832, K=320):
+        return L.dlm_debug_gemm(cfg, epi, sub, tail, group, a, b, c, M, N, K, None)
+    assert call(cfg=999) == dlm.DLM_EINVAL
+    assert call(a=None) == dlm.DLM_EINVAL
+    assert call(K=100) == dlm.DLM_EINVAL
+    assert call(M=0) == dlm.DLM_EINVAL
+    assert call(epi=3) == dlm.DLM_EINVAL
+    assert call(epi=1, N=80) == dlm.DLM_EINVAL           # width 40 not a multiple of 16
+    assert call(cfg=62, epi=1, N=96) == dlm.DLM_EINVAL   # 32x32 tiles: width 48 not a multiple of 32
+    assert call(sub=3, tail=1) == dlm.DLM_EINVAL
+    assert call(cfg=65, sub=2, tail=1) == dlm.DLM_EINVAL  # no sub-tiles for 384x256
+    assert call(sub=4, tail=10 ** 6) == dlm.DLM_EINVAL
+    assert call(tail=-1) == dlm.DLM_EINVAL
+    assert "n_tail" in dlm.last_error()
