@@ -20,7 +20,9 @@ batch of 32).
 
 Prints one JSON line: steps/s (value), unmasked tokens/s, the roofline of the
 dominant kernel (in-library HIP events on the launch stream over the timed
-region), the whole-step roofline, and the CPU oracle timed on a bounded sample.
+region), the whole-step roofline, the latency and roofline of a refresh step
+of the whole batch (timed after the timed region, with a cache), and the CPU
+oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -345,6 +347,10 @@ def main():
                     help="run one tensor-parallel rank's share of the model on this GPU: "
                          "1/N of the query/key-value heads, FFN columns and vocabulary at the "
                          "same rows (the rank's compute only; no collectives)")
+    ap.add_argument("--refresh-steps", type=int, default=None,
+                    help="after the timed steps, time this many steps in which every request "
+                         "refreshes (recomputes its whole sequence); default 2 with a cache, "
+                         "0 without")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the measured MFMA-loop and copy ceilings")
     args = ap.parse_args()
@@ -520,6 +526,41 @@ def main():
     if not args.no_profile:
         dlm.profile_enable(model.handle, False)
         prof = dlm.profile_read(model.handle)
+
+    # refresh steps (every request recomputes its whole sequence), after the
+    # timed region: one untimed, then args.refresh_steps timed one by one
+    n_refresh = args.refresh_steps
+    if n_refresh is None:
+        n_refresh = 0 if w.cache_mode == "none" else 2
+    refresh_step = None
+    if n_refresh > 0:
+        ref_t, ref_F, ref_B, ref_rows = [], 0.0, 0.0, 0
+        for i in range(n_refresh + 1):
+            for b in range(B):
+                if slots[b].done:
+                    eng.release(slots[b])
+                    slots[b] = make(b)
+                    eng.admit(slots[b], cfg.mask_id)
+            rows = [(r.seq_len, r.seq_len) for r in slots]
+            m = sum(r.masked_in_block for r in slots)
+            torch.cuda.synchronize()
+            ts = time.perf_counter()
+            eng.enqueue_step(slots, force_refresh=True)
+            eng.finish_step(slots)
+            dt = time.perf_counter() - ts
+            if i > 0:
+                F, Bb = step_work(shape, rows, m)
+                ref_t.append(dt)
+                ref_F += F
+                ref_B += Bb
+                ref_rows += sum(n for n, _ in rows)
+        t_ref = sum(ref_t) / len(ref_t)
+        pk = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_F32_TFLOPS
+        F1, B1 = ref_F / len(ref_t), ref_B / len(ref_t)
+        refresh_step = {"steps": len(ref_t), "mean_ms": 1e3 * t_ref, "rows": ref_rows / len(ref_t),
+                        "flop": F1, "bytes": B1, "tflops": F1 / t_ref / 1e12,
+                        "frac_mfma": F1 / t_ref / (pk * 1e12),
+                        "frac_hbm": B1 / t_ref / (PEAK_HBM_GBS * 1e9)}
     elapsed = t1 - t0
     t_step = elapsed / args.steps
     peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -612,6 +653,7 @@ def main():
         "class_work": {k: {"flop": f, "bytes": bb} for k, (f, bb) in stats["cls"].items()},
         "step_roofline": step_roof,
         "step_latency": lat,
+        "refresh_step": refresh_step,
         "step_distribution": dist,
         "requests": req,
         "ceilings": ceilings,

@@ -229,8 +229,10 @@ class Engine:
                                   dlm.DLM_REQ_REFRESH if refresh else 0))
         return out
 
-    def enqueue_step(self, reqs: List[Request], stream=None):
-        dreqs = self.dlm_reqs(reqs)
+    def enqueue_step(self, reqs: List[Request], stream=None, force_refresh: bool = False):
+        """Enqueue one step; force_refresh makes it a refresh (recompute) step
+        for every request."""
+        dreqs = self.dlm_reqs(reqs, force_refresh)
         batch = dlm.make_batch(dreqs, self.tokens, self.mask, self.mode_id, self.tok_conf)
         dlm.denoise_step(self.model.handle, self.cache, batch, [r.threshold for r in reqs],
                          self.step_out, self.workspace, stream)
