@@ -302,9 +302,10 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
 
 /* Test hooks for the bf16 GEMM kernel (the contraction of every projection of
  * the step: QKV, output, gate/up and down). dlm_debug_gemm_info: the output
- * tile (bm x bn) of tile configuration cfg and the sub-tile splits it allows
- * for a launch's last round (bit 1: halves, bit 2: quarters); DLM_EINVAL for
- * an unknown configuration. dlm_debug_gemm: one launch of configuration cfg,
+ * tile (bm x bn) of tile configuration cfg and, in *subs, the sub-tile splits
+ * it allows for a launch's last round (bit 1: halves, bit 2: quarters) and
+ * bit 8 when it has no SwiGLU epilogue (its wave tiles hold an odd number of
+ * column fragments); DLM_EINVAL for an unknown configuration. dlm_debug_gemm: one launch of configuration cfg,
  * a [M, K] and b [N, K] bf16, row-major and K-contiguous (device), computing
  * p[m][n] = sum_k a[m][k] b[n][k] in fp32 with the epilogue
  *   0: c [M, N] fp32 = p;
@@ -315,8 +316,8 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
  * sub-tiles (sub 0: whole tiles only); group_m > 0 selects the grouped
  * XCD-aware tile order. DLM_EINVAL (nothing enqueued) for NULL buffers,
  * non-positive sizes, K not a multiple of 64, with epilogue 1 an N/2 that is
- * not a multiple of 16 (of 32 for configurations with 32x32 MFMA tiles), an
- * unknown configuration or epilogue, or a split the configuration does not
+ * not a multiple of 16 (of 32 for configurations with 32x32 MFMA tiles) or a
+ * configuration without it, an unknown configuration or epilogue, or a split the configuration does not
  * allow or with n_tail beyond the tile count. */
 dlm_status dlm_debug_gemm_info(int32_t cfg, int32_t* bm, int32_t* bn, int32_t* subs);
 dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_tail,

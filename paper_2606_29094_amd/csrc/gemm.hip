@@ -231,6 +231,12 @@ const RoundTable kRoundTables[] = {
      {37.4f, 46.5f, 57.2f, 79.0f, 73.6f, 88.7f, 118.5f, 131.5f, 126.5f, 156.3f, 204.0f, 238.4f, 360.9f, 430.0f, 679.5f},
      148},   // measured ahead only with long K walks (the GQA down projection); the
              // table overrates it at 56 k-tiles (4096-row output projection 145 vs 112 us)
+    // 256x224: measured against configuration 6 in the same runs (one and two
+    // full rounds per k-tile count) and scaled by that configuration's table;
+    // a round takes 0.82-0.94 (mean 0.89) of a 256x256 round for 0.875 of its work
+    {70, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {23.2f, 27.2f, 32.7f, 47.2f, 43.6f, 53.5f, 66.8f, 75.0f, 73.5f, 98.5f, 117.1f, 132.5f, 202.1f, 245.6f, 383.7f}},
 };
 
 double round_us(const RoundTable& t, double kt) {
@@ -245,7 +251,7 @@ double round_us(const RoundTable& t, double kt) {
 }  // namespace
 
 GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu, bool allow_mf32,
-                   bool allow_tail) {
+                   bool allow_tail, bool allow_odd) {
   GemmPlan best{-1, 1, 0};
   if (M <= 0 || N <= 0) return best;
   if (es != 2 || K % 64 != 0) {
@@ -263,6 +269,7 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu, boo
   for (const RoundTable& c : kRoundTables) {
     if (M > c.max_m) continue;
     if (!allow_mf32 && gemm_dl_mfma(c.cfg) == 32) continue;
+    if (!allow_odd && gemm_dl_odd(c.cfg)) continue;
     int bm, bn, th;
     gemm_dl_tile(c.cfg, &bm, &bn, &th);
     for (int s = 1; s <= 8; s *= 2) {
@@ -314,7 +321,7 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu, boo
 // 5.8 TB/s).
 GemmPlan lm_head_plan(int es, int M, int V, int K, int num_cu) {
   // the head's epilogue is 16x16 and keeps whole tiles (its partial results are per column tile)
-  GemmPlan p = gemm_plan(es, M, V, K, false, num_cu, false, false);
+  GemmPlan p = gemm_plan(es, M, V, K, false, num_cu, false, false, false);
   if (p.cfg >= 0 && M <= 64) p = GemmPlan{((long)K * es) % 8192 == 0 ? 11 : 10, 1, 0};
   // The head is planned for its largest row count and skips, on the device,
   // the row tiles beyond the rows that need a prediction. The grouped order

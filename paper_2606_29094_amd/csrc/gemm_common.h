@@ -51,6 +51,7 @@ struct EpiStore {
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = true;
   static constexpr bool kTailSplit = true;   // last-round tiles may be split
+  static constexpr bool kOddFragments = true;   // any number of 16-column fragments per wave
   __host__ __device__ void set_mfma(int) {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
@@ -95,6 +96,7 @@ struct EpiScaledStore {
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = false;
   static constexpr bool kTailSplit = false;   // last-round tiles may be split
+  static constexpr bool kOddFragments = true;   // any number of 16-column fragments per wave
   __host__ __device__ void set_mfma(int) {}
   template <int FM, int FN>
   __device__ void op32(f32x16 (&)[FM][FN], int, int, int, int) const {}
@@ -126,6 +128,7 @@ struct EpiAdd {
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = true;
   static constexpr bool kTailSplit = true;   // last-round tiles may be split
+  static constexpr bool kOddFragments = true;   // any number of 16-column fragments per wave
   __host__ __device__ void set_mfma(int) {}
   __device__ int b_row(int n) const { return n; }
   __device__ bool skip_tile(int) const { return false; }
@@ -202,6 +205,7 @@ struct EpiSwiGLU {
   static constexpr bool kRotateK = false;
   static constexpr bool kMf32 = true;
   static constexpr bool kTailSplit = true;   // last-round tiles may be split
+  static constexpr bool kOddFragments = false;  // fragments come in gate/up pairs
   // 32x32 accumulators: tiles fn (gate) and fn + 1 (up) hold the same ffn
   // indices in the same lanes; lanes 0-31 store 32 consecutive outputs of a row
   template <int FM, int FN>
@@ -277,6 +281,7 @@ struct EpiLMHead {
   static constexpr bool kRotateK = true;   // weight streaming: rotate the K walk per column tile
   static constexpr bool kMf32 = false;
   static constexpr bool kTailSplit = false;   // last-round tiles may be split
+  static constexpr bool kOddFragments = true;   // any number of 16-column fragments per wave
   __host__ __device__ void set_mfma(int) {}
   template <int FM, int FN>
   __device__ void op32(f32x16 (&)[FM][FN], int, int, int, int) const {}

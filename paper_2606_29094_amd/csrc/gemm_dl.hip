@@ -42,11 +42,19 @@ __device__ __forceinline__ void dl_tile(char* smem, const bf16* __restrict__ A, 
   constexpr int RPI = 1024 / RB;          // rows per 1 KB wave instruction
   constexpr int KG = RB / 64;             // 32-wide k groups per k-tile
   constexpr int STAGE_A = BM * RB, STAGE_B = BN * RB;
-  constexpr int PERW_A = BM / RPI / NW, PERW_B = BN / RPI / NW;
-  static_assert(PERW_A * NW * RPI == BM && PERW_B * NW * RPI == BN, "rows per wave");
+  // 1 KB instructions per stage, and per wave: an equal share when the count
+  // divides by the waves (wave w takes a contiguous run), else wave w takes
+  // instructions w, w + NW, ... (the first NI % NW waves one more than the rest)
+  constexpr int NI_A = BM / RPI, NI_B = BN / RPI;
+  static_assert(NI_A * RPI == BM && NI_B * RPI == BN, "rows per instruction");
+  constexpr bool EVEN_A = NI_A % NW == 0, EVEN_B = NI_B % NW == 0;
+  constexpr int PERW_A = (NI_A + NW - 1) / NW, PERW_B = (NI_B + NW - 1) / NW;
+  constexpr int MINW_A = NI_A / NW, MINW_B = NI_B / NW;
   // loads of a wave that may stay in flight at the top of an iteration: those
-  // issued after A(kt) in the steady issue order (see the pipeline below)
-  constexpr int INFLIGHT = DB > DA ? DA * PERW_B + (DA - 1) * PERW_A : (DA - 1) * (PERW_A + PERW_B);
+  // issued after A(kt) in the steady issue order (see the pipeline below),
+  // counted for the waves with the fewest (a wave with more then waits for
+  // one or two of the next k-tile's loads too, which is safe)
+  constexpr int INFLIGHT = DB > DA ? DA * MINW_B + (DA - 1) * MINW_A : (DA - 1) * (MINW_A + MINW_B);
   static_assert(INFLIGHT < 64, "vmcnt range");
   char* const smem_b = smem + SA * STAGE_A;
 
@@ -76,35 +84,42 @@ __device__ __forceinline__ void dl_tile(char* smem, const bf16* __restrict__ A, 
   // source of this lane for each of its wave's instructions (fixed over k),
   // as 32-bit element offsets from the matrix base (operands hold fewer than
   // 2^31 elements; half the registers of 64-bit pointers)
+  // stage instruction of this wave's j-th load, and whether the wave has one
+  auto inst_a = [&](int j) { return EVEN_A ? wave * PERW_A + j : wave + j * NW; };
+  auto inst_b = [&](int j) { return EVEN_B ? wave * PERW_B + j : wave + j * NW; };
+  auto has_a = [&](int j) { return j < MINW_A || inst_a(j) < NI_A; };
+  auto has_b = [&](int j) { return j < MINW_B || inst_b(j) < NI_B; };
   uint32_t srcA[PERW_A];
   uint32_t srcB[PERW_B];
 #pragma unroll
   for (int j = 0; j < PERW_A; ++j) {
-    const int row = RPI * (wave * PERW_A + j) + lane / CPR;
+    const int row = RPI * inst_a(j) + lane / CPR;
     const int cc = (lane % CPR) ^ swz(row);
     srcA[j] = (uint32_t)min(m0 + row, M - 1) * (uint32_t)lda + kbeg + cc * 8;
   }
 #pragma unroll
   for (int j = 0; j < PERW_B; ++j) {
-    const int row = RPI * (wave * PERW_B + j) + lane / CPR;
+    const int row = RPI * inst_b(j) + lane / CPR;
     const int cc = (lane % CPR) ^ swz(row);
     srcB[j] = (uint32_t)epi.b_row(min(n0 + row, N - 1)) * (uint32_t)ldb + kbeg + cc * 8;
   }
   auto issue_a = [&](int stage, int kt) {
-    char* dst = smem + stage * STAGE_A + wave * PERW_A * 1024;
+    char* dst = smem + stage * STAGE_A;
     const bf16* base = A + kt * BK;
 #pragma unroll
     for (int j = 0; j < PERW_A; ++j)
-      __builtin_amdgcn_global_load_lds((gptr_t)(base + srcA[j]), (lptr_t)(dst + j * 1024), 16,
-                                       0, 0);
+      if (has_a(j))
+        __builtin_amdgcn_global_load_lds((gptr_t)(base + srcA[j]),
+                                         (lptr_t)(dst + inst_a(j) * 1024), 16, 0, 0);
   };
   auto issue_b = [&](int stage, int kt) {
-    char* dst = smem_b + stage * STAGE_B + wave * PERW_B * 1024;
+    char* dst = smem_b + stage * STAGE_B;
     const bf16* base = B + kt * BK;
 #pragma unroll
     for (int j = 0; j < PERW_B; ++j)
-      __builtin_amdgcn_global_load_lds((gptr_t)(base + srcB[j]), (lptr_t)(dst + j * 1024), 16,
-                                       0, 0);
+      if (has_b(j))
+        __builtin_amdgcn_global_load_lds((gptr_t)(base + srcB[j]),
+                                         (lptr_t)(dst + inst_b(j) * 1024), 16, 0, 0);
   };
 
   // accumulators: 16x16 tiles (4 values per lane) or 32x32 tiles (16 per lane)
@@ -406,7 +421,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
 }
 
 // Tile configurations (BM, BN, waves M x N, activation stages, weight stages,
-// k-tile row bytes, MFMA tile 16x16x32 or 32x32x16).
+// k-tile row bytes, MFMA tile 16x16x32 or 32x32x16). 256x224 (wave tiles of
+// 64x112, seven column fragments) covers a 3584-wide output in 16 column
+// tiles, so that 4096 rows make exactly one round of 256 tiles.
 #define DL_CONFIGS(X)                   \
   X(1, 128, 128, 2, 2, 2, 2, 128, 16)   \
   X(6, 256, 256, 2, 4, 2, 2, 128, 16)   \
@@ -418,7 +435,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   X(42, 128, 192, 2, 2, 2, 3, 128, 16)  \
   X(43, 256, 128, 4, 2, 2, 4, 128, 16)  \
   X(62, 256, 128, 2, 2, 2, 2, 128, 32)  \
-  X(65, 384, 256, 4, 2, 2, 2, 128, 32)
+  X(65, 384, 256, 4, 2, 2, 2, 128, 32)  \
+  X(70, 256, 224, 4, 2, 2, 2, 128, 16)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
@@ -434,6 +452,18 @@ int gemm_dl_mfma(int cfg) {
   switch (cfg) {
 #define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_) \
   case id: return MF_;
+    DL_CONFIGS(X)
+#undef X
+  }
+  return 0;
+}
+
+// Whether a wave's tile holds an odd number of MFMA column fragments (the
+// SwiGLU epilogue, which stores gate/up fragment pairs, cannot run it).
+int gemm_dl_odd(int cfg) {
+  switch (cfg) {
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_) \
+  case id: return (BN_ / WN_ / MF_) % 2;
     DL_CONFIGS(X)
 #undef X
   }
@@ -471,7 +501,9 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
   switch (cfg) {
 #define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                                        \
   case id: {                                                                             \
-    if constexpr (MF_ == 32 && !Epi::kMf32) return hipErrorInvalidValue;                 \
+    if constexpr ((MF_ == 32 && !Epi::kMf32) ||                                          \
+                  (!Epi::kOddFragments && (BN_ / WN_ / MF_) % 2 != 0))                   \
+      return hipErrorInvalidValue;                                                       \
     else {                                                                               \
       const int n_n = ceil_div(N, BN_), n_m = ceil_div(M, BM_);                          \
       const long total = (long)n_n * n_m * splits;                                       \

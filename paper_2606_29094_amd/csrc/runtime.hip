@@ -196,7 +196,7 @@ Layout layout(const dlm_model* m, int n, int n_req) {
   L.g_o = gemm_plan(es_i, n, c.d_model, qd, true, m->num_cu);
   // the SwiGLU GEMM keeps 16x16 tiles: its 32x32 variants measured 5-6 %
   // slower on every gate/up shape
-  L.g_gu = gemm_plan(es_i, n, 2 * c.d_ffn, c.d_model, false, m->num_cu, false);
+  L.g_gu = gemm_plan(es_i, n, 2 * c.d_ffn, c.d_model, false, m->num_cu, false, true, false);
   L.g_down = gemm_plan(es_i, n, c.d_model, c.d_ffn, true, m->num_cu);
   L.m_max = std::min(n, n_req * kMaxBlock);
   L.g_lm = lm_head_plan(es_i, L.m_max, c.vocab, c.d_model, m->num_cu);
@@ -811,7 +811,7 @@ dlm_status dlm_debug_gemm_info(int32_t cfg, int32_t* bm, int32_t* bn, int32_t* s
   if (!gemm_dl_tile(cfg, &tm, &tn, &th)) return fail(DLM_EINVAL, "no GEMM configuration %d", cfg);
   if (bm) *bm = tm;
   if (bn) *bn = tn;
-  if (subs) *subs = gemm_dl_subs(cfg);
+  if (subs) *subs = gemm_dl_subs(cfg) | (gemm_dl_odd(cfg) ? 8 : 0);
   return DLM_OK;
 }
 
@@ -831,6 +831,8 @@ dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_
   const int pair = gemm_dl_mfma(cfg) == 32 ? 32 : 16;
   if (epilogue == 1 && (N / 2) % pair != 0)
     return fail(DLM_EINVAL, "SwiGLU width %d is not a multiple of %d", N / 2, pair);
+  if (epilogue == 1 && gemm_dl_odd(cfg))
+    return fail(DLM_EINVAL, "configuration %d has no SwiGLU epilogue (odd fragment count)", cfg);
   if (sub != 0 && ((sub != 2 && sub != 4) || !(gemm_dl_subs(cfg) & sub)))
     return fail(DLM_EINVAL, "configuration %d has no %d-way sub-tiles", cfg, sub);
   if (sub != 0 && (long)n_tail > (long)ceil_div(M, tm) * ceil_div(N, tn))

@@ -264,8 +264,9 @@ def head_confidence(model, u_rows, m_rows: int, conf, tok, workspace, stream=Non
 
 
 def debug_gemm_info(cfg: int):
-    """(bm, bn, allowed sub-tile splits bitmask) of a GEMM tile configuration,
-    or None when the configuration does not exist."""
+    """(bm, bn, flags) of a GEMM tile configuration, or None when the
+    configuration does not exist; flags: bit 1 / bit 2 allowed half / quarter
+    sub-tiles, bit 8 no SwiGLU epilogue."""
     bm, bn, subs = c_int32(), c_int32(), c_int32()
     rc = lib().dlm_debug_gemm_info(cfg, ctypes.byref(bm), ctypes.byref(bn), ctypes.byref(subs))
     if rc != DLM_OK:

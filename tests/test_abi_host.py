@@ -252,6 +252,8 @@ def test_debug_gemm_validation_on_host():
     assert (bm.value, bn.value, subs.value) == (256, 256, 6)      # halves and quarters
     assert L.dlm_debug_gemm_info(65, ctypes.byref(bm), ctypes.byref(bn), ctypes.byref(subs)) == 0
     assert (bm.value, bn.value, subs.value) == (384, 256, 0)
+    assert L.dlm_debug_gemm_info(70, ctypes.byref(bm), ctypes.byref(bn), ctypes.byref(subs)) == 0
+    assert (bm.value, bn.value, subs.value) == (256, 224, 8)      # seven fragments: no SwiGLU
     assert L.dlm_debug_gemm_info(999, None, None, None) == dlm.DLM_EINVAL
     F = FAKE
 
@@ -264,6 +266,8 @@ def test_debug_gemm_validation_on_host():
     assert call(epi=3) == dlm.DLM_EINVAL
     assert call(epi=1, N=80) == dlm.DLM_EINVAL           # width 40 not a multiple of 16
     assert call(cfg=62, epi=1, N=96) == dlm.DLM_EINVAL   # 32x32 tiles: width 48 not a multiple of 32
+    assert call(cfg=70, epi=1) == dlm.DLM_EINVAL          # odd fragment count: no SwiGLU
+    assert "SwiGLU" in dlm.last_error()
     assert call(sub=3, tail=1) == dlm.DLM_EINVAL
     assert call(cfg=65, sub=2, tail=1) == dlm.DLM_EINVAL  # no sub-tiles for 384x256
     assert call(sub=4, tail=10 ** 6) == dlm.DLM_EINVAL

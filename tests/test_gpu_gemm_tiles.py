@@ -49,6 +49,7 @@ def test_configurations_exist(gpu):
     cfgs = _configs()
     assert len(cfgs) >= 8
     assert any(s & 4 for _, _, _, s in cfgs) and any(s & 2 for _, _, _, s in cfgs)
+    assert any(s & 8 for _, _, _, s in cfgs)
 
 
 @pytest.mark.parametrize("cfg,bm,bn,subs", _configs(), ids=lambda v: str(v))
@@ -67,8 +68,13 @@ def test_whole_tiles_match_fp64_product(gpu, cfg, bm, bn, subs):
     c = _run(gpu, cfg, 2, a_d, b_d, c0.to(gpu)).cpu().double().numpy()
     ref = c0.double().numpy() + P
     assert np.all(np.abs(c - ref) <= tol + U * np.abs(ref)), cfg
-    # SwiGLU: silu(gate) * up, rounded to bf16
+    # SwiGLU: silu(gate) * up, rounded to bf16 (configurations whose wave
+    # tiles hold an odd number of column fragments reject it)
     F = N // 2
+    if subs & 8:
+        with pytest.raises(dlm.DlmError):
+            _run(gpu, cfg, 1, a_d, b_d, torch.zeros(M, F, dtype=torch.bfloat16, device=gpu))
+        return
     y = _run(gpu, cfg, 1, a_d, b_d, torch.zeros(M, F, dtype=torch.bfloat16, device=gpu))
     y = y.cpu().double().numpy()
     g, u = P[:, :F], P[:, F:]
@@ -87,18 +93,20 @@ def _split_cases():
     for cfg, bm, bn, subs in _configs():
         for sub in (2, 4):
             if subs & sub:
-                out.append((cfg, bm, bn, sub))
+                out.append((cfg, bm, bn, sub, subs))
     return out
 
 
-@pytest.mark.parametrize("cfg,bm,bn,sub", _split_cases(), ids=lambda v: str(v))
-def test_sub_tiles_equal_whole_tiles_bitwise(gpu, cfg, bm, bn, sub):
+@pytest.mark.parametrize("cfg,bm,bn,sub,subs", _split_cases(), ids=lambda v: str(v))
+def test_sub_tiles_equal_whole_tiles_bitwise(gpu, cfg, bm, bn, sub, subs):
     M, N, K = _shape(bm, bn)
     tiles = -(-M // bm) * -(-N // bn)
     a, b, a_d, b_d = _operands(gpu, M, N, K, seed=100 + cfg)
     c0 = torch.randn(M, N, generator=torch.Generator().manual_seed(8)).to(gpu)
-    for epi, init in ((0, torch.zeros(M, N, device=gpu)), (2, c0),
-                      (1, torch.zeros(M, N // 2, dtype=torch.bfloat16, device=gpu))):
+    epis = [(0, torch.zeros(M, N, device=gpu)), (2, c0)]
+    if not subs & 8:
+        epis.append((1, torch.zeros(M, N // 2, dtype=torch.bfloat16, device=gpu)))
+    for epi, init in epis:
         for group_m in (0, 2):
             whole = _run(gpu, cfg, epi, a_d, b_d, init, group_m=group_m)
             for n_tail in (1, 3, tiles):
