@@ -308,21 +308,24 @@ dlm_status dlm_head_confidence(dlm_model* m, const void* u_rows, int32_t m_rows,
  * column fragments); DLM_EINVAL for an unknown configuration. dlm_debug_gemm: one launch of configuration cfg,
  * a [M, K] and b [N, K] bf16, row-major and K-contiguous (device), computing
  * p[m][n] = sum_k a[m][k] b[n][k] in fp32 with the epilogue
- *   0: c [M, N] fp32 = p;
+ *   0: c [splits, M, N] fp32, slice z = the sum over k in
+ *      [z K / splits, (z + 1) K / splits) (the whole p when splits is 1);
  *   1: c [M, N/2] bf16 = silu(g) * u with g = p[:, f], u = p[:, N/2 + f]
  *      (rows [0, N/2) of b are the gate weights, [N/2, N) the up weights);
  *   2: c [M, N] fp32 += p;
  * the last n_tail tiles of the launch's tile order run as `sub` (2 or 4)
  * sub-tiles (sub 0: whole tiles only); group_m > 0 selects the grouped
  * XCD-aware tile order. DLM_EINVAL (nothing enqueued) for NULL buffers,
- * non-positive sizes, K not a multiple of 64, with epilogue 1 an N/2 that is
- * not a multiple of 16 (of 32 for configurations with 32x32 MFMA tiles) or a
- * configuration without it, an unknown configuration or epilogue, or a split the configuration does not
- * allow or with n_tail beyond the tile count. */
+ * non-positive sizes, K not a multiple of 64, splits below 1, above 1 with
+ * epilogue 1 or 2, or not dividing the K/64 k-tiles, with epilogue 1 an N/2
+ * that is not a multiple of 16 (of 32 for configurations with 32x32 MFMA
+ * tiles) or a configuration without it, an unknown configuration or
+ * epilogue, or a sub-tile split the configuration does not allow or with
+ * n_tail beyond the tile count. */
 dlm_status dlm_debug_gemm_info(int32_t cfg, int32_t* bm, int32_t* bn, int32_t* subs);
 dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_tail,
-                          int32_t group_m, const void* a, const void* b, void* c, int32_t M,
-                          int32_t N, int32_t K, void* stream);
+                          int32_t group_m, int32_t splits, const void* a, const void* b, void* c,
+                          int32_t M, int32_t N, int32_t K, void* stream);
 
 /* Kernel timing. While enabled, every kernel the library enqueues for this
  * model (or, when only_class is not NULL, every kernel of that class; see also

@@ -367,12 +367,14 @@ hipError_t gemm_swiglu(const GemmPlan& p, const T* A, int lda, const T* W, int l
 }
 
 hipError_t gemm_debug_launch(int cfg, int epilogue, int sub, int n_tail, int group_m,
-                             const bf16* A, const bf16* B, void* C, int M, int N, int K,
-                             hipStream_t st) {
+                             int splits, const bf16* A, const bf16* B, void* C, int M, int N,
+                             int K, hipStream_t st) {
   if (epilogue == 0) {
     EpiStore e{reinterpret_cast<float*>(C), N, (long)M * N, M, N};
-    return gemm_dl_launch<EpiStore>(cfg, A, K, B, K, M, N, K, 1, group_m, sub, n_tail, e, st);
+    return gemm_dl_launch<EpiStore>(cfg, A, K, B, K, M, N, K, splits, group_m, sub, n_tail, e,
+                                    st);
   }
+  if (splits != 1) return hipErrorInvalidValue;
   if (epilogue == 1) {
     EpiSwiGLU<bf16> e{reinterpret_cast<bf16*>(C), N / 2, M, N / 2};
     return gemm_dl_launch<EpiSwiGLU<bf16>>(cfg, A, K, B, K, M, N, K, 1, group_m, sub, n_tail, e,

@@ -65,11 +65,12 @@ int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads);
 int gemm_dl_mfma(int cfg);
 int gemm_dl_subs(int cfg);
 int gemm_dl_odd(int cfg);
-// one launch of configuration cfg with epilogue 0 (fp32 store), 1 (SwiGLU to
-// bf16, N = 2 F) or 2 (fp32 add), A [M, K], B [N, K], C row-major (test hook)
+// one launch of configuration cfg with epilogue 0 (fp32 store of `splits` K
+// slices), 1 (SwiGLU to bf16, N = 2 F) or 2 (fp32 add), A [M, K], B [N, K],
+// C row-major (test hook)
 hipError_t gemm_debug_launch(int cfg, int epilogue, int sub, int n_tail, int group_m,
-                             const bf16* A, const bf16* B, void* C, int M, int N, int K,
-                             hipStream_t st);
+                             int splits, const bf16* A, const bf16* B, void* C, int M, int N,
+                             int K, hipStream_t st);
 // allow_tail: the last round may be split into sub-tiles (epilogues that allow it)
 // allow_odd: configurations whose wave tiles hold an odd number of column
 // fragments may be chosen (every epilogue but SwiGLU)

@@ -816,8 +816,8 @@ dlm_status dlm_debug_gemm_info(int32_t cfg, int32_t* bm, int32_t* bn, int32_t* s
 }
 
 dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_tail,
-                          int32_t group_m, const void* a, const void* b, void* c, int32_t M,
-                          int32_t N, int32_t K, void* stream) {
+                          int32_t group_m, int32_t splits, const void* a, const void* b, void* c,
+                          int32_t M, int32_t N, int32_t K, void* stream) {
   g_err.clear();
   if (!a || !b || !c) return fail(DLM_EINVAL, "NULL buffer");
   if (M < 1 || N < 1 || K < 1 || K % 64 != 0)
@@ -825,6 +825,9 @@ dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_
   if (epilogue < 0 || epilogue > 2) return fail(DLM_EINVAL, "epilogue %d", epilogue);
   if (epilogue == 1 && N % 2 != 0) return fail(DLM_EINVAL, "odd N %d for the SwiGLU epilogue", N);
   if (group_m < 0 || n_tail < 0) return fail(DLM_EINVAL, "negative group_m or n_tail");
+  if (splits < 1 || (splits > 1 && epilogue != 0) || (K / 64) % splits != 0)
+    return fail(DLM_EINVAL, "splits %d (K slices of the plain store only, dividing the %d k-tiles)",
+                splits, K / 64);
   int tm = 0, tn = 0, th = 0;
   if (!gemm_dl_tile(cfg, &tm, &tn, &th)) return fail(DLM_EINVAL, "no GEMM configuration %d", cfg);
   // the gate/up interleave pairs columns in groups of the MFMA tile width
@@ -837,7 +840,7 @@ dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_
     return fail(DLM_EINVAL, "configuration %d has no %d-way sub-tiles", cfg, sub);
   if (sub != 0 && (long)n_tail > (long)ceil_div(M, tm) * ceil_div(N, tn))
     return fail(DLM_EINVAL, "n_tail %d beyond the tile count", n_tail);
-  const hipError_t e = gemm_debug_launch(cfg, epilogue, sub, n_tail, group_m,
+  const hipError_t e = gemm_debug_launch(cfg, epilogue, sub, n_tail, group_m, splits,
                                          reinterpret_cast<const bf16*>(a),
                                          reinterpret_cast<const bf16*>(b), c, M, N, K,
                                          reinterpret_cast<hipStream_t>(stream));

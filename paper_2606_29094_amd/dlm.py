@@ -121,8 +121,9 @@ def lib():
                                           c_void_p, c_size_t, c_void_p]
         L.dlm_debug_gemm_info.argtypes = [c_int32, POINTER(c_int32), POINTER(c_int32),
                                           POINTER(c_int32)]
-        L.dlm_debug_gemm.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p,
-                                     c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p]
+        L.dlm_debug_gemm.argtypes = [c_int32, c_int32, c_int32, c_int32, c_int32, c_int32,
+                                     c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32,
+                                     c_void_p]
         L.dlm_profile_enable.argtypes = [c_void_p, c_int32, ctypes.c_char_p]
         L.dlm_profile_read.argtypes = [c_void_p, POINTER(DlmProfileEntry), c_int32,
                                        POINTER(c_int32)]
@@ -275,9 +276,10 @@ def debug_gemm_info(cfg: int):
 
 
 def debug_gemm(cfg: int, epilogue: int, a, b, c, sub: int = 0, n_tail: int = 0,
-               group_m: int = 0, stream=None):
-    """One launch of GEMM configuration cfg: epilogue 0 stores a @ b.T (fp32),
-    1 stores silu(gate) * up (bf16, N/2 columns), 2 adds a @ b.T into c."""
+               group_m: int = 0, splits: int = 1, stream=None):
+    """One launch of GEMM configuration cfg: epilogue 0 stores a @ b.T (fp32;
+    with splits > 1 one slice per K range, c of shape (splits, M, N)), 1 stores
+    silu(gate) * up (bf16, N/2 columns), 2 adds a @ b.T into c."""
     M, K = a.shape
     N = b.shape[0]
     for t in (a, b, c):
@@ -285,11 +287,11 @@ def debug_gemm(cfg: int, epilogue: int, a, b, c, sub: int = 0, n_tail: int = 0,
             raise ValueError("GEMM operands must be contiguous")
     if b.shape[1] != K:
         raise ValueError("a and b disagree on K")
-    want = (M, N // 2) if epilogue == 1 else (M, N)
+    want = (M, N // 2) if epilogue == 1 else ((splits, M, N) if splits > 1 else (M, N))
     if tuple(c.shape) != want:
         raise ValueError(f"c has shape {tuple(c.shape)}, expected {want}")
-    check(lib().dlm_debug_gemm(cfg, epilogue, sub, n_tail, group_m, _ptr(a), _ptr(b), _ptr(c),
-                               M, N, K, _stream(stream)))
+    check(lib().dlm_debug_gemm(cfg, epilogue, sub, n_tail, group_m, splits, _ptr(a), _ptr(b),
+                               _ptr(c), M, N, K, _stream(stream)))
 
 
 def profile_enable(model, on: bool, only_class: str | None = None):

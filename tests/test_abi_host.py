@@ -257,8 +257,8 @@ def test_debug_gemm_validation_on_host():
     assert L.dlm_debug_gemm_info(999, None, None, None) == dlm.DLM_EINVAL
     F = FAKE
 
-    def call(cfg=6, epi=0, sub=0, tail=0, group=0, a=F, b=F, c=F, M=300, N=832, K=320):
-        return L.dlm_debug_gemm(cfg, epi, sub, tail, group, a, b, c, M, N, K, None)
+    def call(cfg=6, epi=0, sub=0, tail=0, group=0, a=F, b=F, c=F, M=300, N=832, K=320, splits=1):
+        return L.dlm_debug_gemm(cfg, epi, sub, tail, group, splits, a, b, c, M, N, K, None)
     assert call(cfg=999) == dlm.DLM_EINVAL
     assert call(a=None) == dlm.DLM_EINVAL
     assert call(K=100) == dlm.DLM_EINVAL
@@ -273,3 +273,7 @@ def test_debug_gemm_validation_on_host():
     assert call(sub=4, tail=10 ** 6) == dlm.DLM_EINVAL
     assert call(tail=-1) == dlm.DLM_EINVAL
     assert "n_tail" in dlm.last_error()
+    assert call(splits=0) == dlm.DLM_EINVAL
+    assert call(splits=2) == dlm.DLM_EINVAL               # 5 k-tiles do not split in two
+    assert "splits" in dlm.last_error()
+    assert call(epi=2, splits=5) == dlm.DLM_EINVAL        # slices of the plain store only

@@ -2,10 +2,11 @@
 (dlm_debug_gemm): every tile configuration, with whole tiles, against the
 fp64 product of the same bf16 operands (plain store, residual add and the
 SwiGLU epilogue, the feed-forward of "Background and Challenges", Diffusion
-Language Models), and, for every last-round sub-tile split a configuration
-allows, bit for bit against its whole-tile launch (sub-tiles accumulate each
-output element over the same k order). Shapes span several tiles with ragged
-row and column tails."""
+Language Models), its K-split slices against the fp64 partial products, and,
+for every last-round sub-tile split a configuration allows, bit for bit
+against its whole-tile launch (sub-tiles accumulate each output element over
+the same k order). Shapes span several tiles with ragged row and column
+tails."""
 import numpy as np
 import pytest
 import torch
@@ -86,6 +87,30 @@ def test_whole_tiles_match_fp64_product(gpu, cfg, bm, bn, subs):
         + tol[:, :F] * tol[:, F:] + 8 * U * np.abs(ref)
     err = half_ulp(np.abs(ref) + slack, "bf16") + slack
     assert np.all(np.abs(y - ref) <= err), (cfg, float(np.max(np.abs(y - ref) / err)))
+
+
+@pytest.mark.parametrize("cfg,bm,bn,subs", _configs(), ids=lambda v: str(v))
+def test_k_slices_match_fp64_partial_products(gpu, cfg, bm, bn, subs):
+    """K-split launches (the plain fp32 store of one slice per K range, which
+    the RoPE kernel or the residual norm sums): every slice against the fp64
+    product over its own k range, for 2, 4 and 8 slices of 8 k-tiles, in both
+    tile orders; slices start as NaN, so an unwritten element fails."""
+    M, N, K = _shape(bm, bn, K=512)
+    a, b, a_d, b_d = _operands(gpu, M, N, K, seed=200 + cfg)
+    A = a.double().numpy()
+    B = b.double().numpy()
+    for s in (2, 4, 8):
+        w = K // s
+        parts = [A[:, z * w:(z + 1) * w] @ B[:, z * w:(z + 1) * w].T for z in range(s)]
+        tols = [gemm_tol(A[:, z * w:(z + 1) * w], B[:, z * w:(z + 1) * w], 1, "bf16")
+                for z in range(s)]
+        for group_m in (0, 2):
+            c = torch.full((s, M, N), float("nan"), device=gpu)
+            dlm.debug_gemm(cfg, 0, a_d, b_d, c, group_m=group_m, splits=s)
+            torch.cuda.synchronize()
+            c = c.cpu().double().numpy()
+            for z in range(s):
+                assert np.all(np.abs(c[z] - parts[z]) <= tols[z]), (cfg, s, group_m, z)
 
 
 def _split_cases():
