@@ -254,7 +254,10 @@ __global__ __launch_bounds__(NTH) void qkv_rope_scatter_kernel(
   constexpr int HALF = DH / 2;
   __shared__ T vt[DH][kQTile + 2];
   const int tile = blockIdx.x;
-  const int y = blockIdx.y;
+  // head slots in reverse dispatch order: the key/value blocks (rotation, value
+  // transpose and two stores: the longest) start first instead of forming the
+  // launch's last wave (GQA 64-request cache step 41 -> 35 us)
+  const int y = (int)gridDim.y - 1 - (int)blockIdx.y;
   const int r = plan_req_of_tile(p, tile);
   const ReqPlan& q = p.r[r];
   const int lrow0 = (tile - q.tile0) * kQTile;           // first row within request
