@@ -29,6 +29,25 @@
 
 namespace dlm {
 
+// P split into hi + lo bf16 terms (p = hi + lo to about 16 significant bits)
+// for the eight probabilities a lane feeds one PV MFMA: lo = bf16(p - hi),
+// converted two at a time (one packed conversion per pair for each term)
+__device__ __forceinline__ void split_p8(const f32x4& a, const f32x4& b, bf16x8& ph, bf16x8& pl) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const f32x2_t v = e < 2 ? f32x2_t{a[2 * e], a[2 * e + 1]} : f32x2_t{b[2 * e - 4], b[2 * e - 3]};
+    const bf16x2_t h = __builtin_convertvector(v, bf16x2_t);
+    const bf16x2_t l = __builtin_convertvector(v - __builtin_convertvector(h, f32x2_t), bf16x2_t);
+    ph[2 * e] = h[0];
+    ph[2 * e + 1] = h[1];
+    pl[2 * e] = l[0];
+    pl[2 * e + 1] = l[1];
+  }
+}
+
+
 constexpr int kKeyTile = 64;
 
 // Wave layout: QG query groups of 16 rows x KG key groups. A block stages
@@ -233,12 +252,7 @@ __global__ __launch_bounds__(QG* KG * 64) void attn_bf16_kernel(StepPlan p, cons
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       bf16x8 ph, pl;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pv = e < 4 ? sblk[2 * j][e] : sblk[2 * j + 1][e - 4];
-        ph[e] = (bf16)pv;
-        pl[e] = (bf16)(pv - (float)ph[e]);
-      }
+      split_p8(sblk[2 * j], sblk[2 * j + 1], ph, pl);
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const bf16* vrow = vs + (db * 16 + (lane & 15)) * VS + kg * 64 + 32 * j + 8 * g;
@@ -520,12 +534,7 @@ __global__ __launch_bounds__(GH* QG * 64) void attn_gqa_kernel(StepPlan p, const
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       bf16x8 ph, pl;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pv = e < 4 ? sblk[2 * j][e] : sblk[2 * j + 1][e - 4];
-        ph[e] = (bf16)pv;
-        pl[e] = (bf16)(pv - (float)ph[e]);
-      }
+      split_p8(sblk[2 * j], sblk[2 * j + 1], ph, pl);
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const u32x4 a = *reinterpret_cast<const u32x4*>(vst + (db * 16 + (lane & 15)) * 128 +
