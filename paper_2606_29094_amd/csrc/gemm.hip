@@ -330,6 +330,9 @@ GemmPlan lm_head_plan(int es, int M, int V, int K, int num_cu) {
   // (half the XCDs idle with two groups).
   int bm, bn, th;
   if (p.group_m > 0 && gemm_dl_tile(p.cfg, &bm, &bn, &th)) p.group_m = ceil_div(M, bm);
+  // over several row tiles, walk only the tiles of the rows that need a prediction
+  if (p.cfg >= 0 && gemm_dl_tile(p.cfg, &bm, &bn, &th) && ceil_div(M, bm) > 1)
+    p.active_cus = num_cu;
   return p;
 }
 
@@ -399,6 +402,10 @@ hipError_t gemm_lm_head(const GemmPlan& p, const T* U, int ldu, const T* W, int 
                         const int* m_count, hipStream_t st) {
   if (p.splits != 1) return hipErrorInvalidValue;
   EpiLMHead e{pm, ps, pi, M, V, inv_tau, ld, m_count};
+  if constexpr (sizeof(T) == 2) {
+    if (p.cfg >= 0 && p.active_cus > 0)
+      return gemm_dl_head_launch(p.cfg, U, ldu, W, K, M, V, K, p.active_cus, e, st);
+  }
   return launch<T>(p, U, ldu, W, K, M, V, K, e, st);
 }
 

@@ -420,6 +420,36 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
                                                           tz, kbeg, kend, epi);
 }
 
+// LM head over the rows that need a prediction only. The head is planned for
+// its largest row count and the count of rows that need a prediction is
+// known on the device only; one block per tile would dispatch every tile and
+// let those beyond the count exit, and in the grouped order such skipped
+// blocks come in runs between the active ones of each column tile (18-23 %
+// of the launch at ~1400 of 4096 rows). Here each XCD's blocks (linear block
+// i runs on XCD i mod 8) walk the active tiles of the XCD's contiguous range
+// of column tiles, the rows of one column tile on consecutive blocks, so
+// those share the column's weight tile in L2 at about the same time, as in
+// the grouped order. No block waits on another.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF>
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_head_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
+    int K, int n_n, EpiLMHead epi) {
+  __shared__ __attribute__((aligned(1024))) char smem[(SA * BM + SB * BN) * RB];
+  const int rows = epi.m_count ? min(*epi.m_count, M) : M;
+  const int act = rows > 0 ? (rows + BM - 1) / BM : 0;     // active row tiles
+  const int xcd = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
+  const int nbx = ((int)gridDim.x - xcd + kXcds - 1) / kXcds;   // blocks on this XCD
+  const int c0 = (int)((long)n_n * xcd / kXcds), c1 = (int)((long)n_n * (xcd + 1) / kXcds);
+  const int total = (c1 - c0) * act;
+  for (int a = k; a < total; a += nbx) {
+    const int c = a / act;
+    const int tn = c0 + c, tm = a - c * act;
+    dl_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, EpiLMHead>(
+        smem, A, lda, B, ldb, M, N, tm * BM, tn * BN, tn, 0, 0, K, epi);
+    __syncthreads();   // the epilogue's LDS reads before the next tile's loads
+  }
+}
+
 // Tile configurations (BM, BN, waves M x N, activation stages, weight stages,
 // k-tile row bytes, MFMA tile 16x16x32 or 32x32x16). 256x224 (wave tiles of
 // 64x112, seven column fragments) covers a 3584-wide output in 16 column
@@ -523,6 +553,34 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
       }                                                                                  \
       return hipGetLastError();                                                          \
     }                                                                                    \
+  }
+    DL_CONFIGS(X)
+#undef X
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t gemm_dl_head_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M,
+                               int N, int K, int num_cu, const EpiLMHead& epi, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (K % 64 != 0 || num_cu < kXcds) return hipErrorInvalidValue;
+  if ((double)(M - 1) * lda + K >= 4294967296.0 || (double)(N - 1) * ldb + K >= 4294967296.0)
+    return hipErrorInvalidValue;
+  switch (cfg) {
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                                         \
+  case id: {                                                                              \
+    if constexpr (MF_ == 32) return hipErrorInvalidValue;                                 \
+    else {                                                                                \
+      /* blocks per CU: bounded by the LDS (160 KB) and by 32 waves per CU */              \
+      constexpr int kLds = (SA_ * BM_ + S_ * BN_) * RB_, kWaves = WM_ * WN_;              \
+      constexpr int kOcc = 163840 / kLds < 32 / kWaves ? 163840 / kLds : 32 / kWaves;     \
+      EpiLMHead e = epi;                                                                  \
+      e.set_mfma(MF_);                                                                    \
+      DLM_LAUNCH((gemm_dl_head_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_>),            \
+                 dim3(num_cu * (kOcc > 0 ? kOcc : 1)), dim3(kWaves * 64), 0, st, A, lda, B, \
+                 ldb, M, N, K, ceil_div(N, BN_), e);                                      \
+      return hipGetLastError();                                                           \
+    }                                                                                     \
   }
     DL_CONFIGS(X)
 #undef X

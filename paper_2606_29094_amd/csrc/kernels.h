@@ -50,8 +50,11 @@ __device__ __forceinline__ int plan_req_of_tile(const StepPlan& p, int tile) {
 // cfg >= 0: a direct-load tile configuration (bf16); cfg < 0: register-staged
 // kernel. splits: number of K slices (fp32 partial slices, summed by the consumer).
 // group_m: tile order (0 = plain); sub, n_tail: the last n_tail tiles of the
-// order are each run as `sub` (2 or 4) sub-tiles (0: none)
-struct GemmPlan { int cfg; int splits; int group_m; int sub = 0; int n_tail = 0; };
+// order are each run as `sub` (2 or 4) sub-tiles (0: none); active_cus > 0
+// (LM head over several row tiles only): one launch of blocks on that many
+// CUs that walk the tiles of the rows needing a prediction (see
+// gemm_dl_head_launch) instead of one block per tile
+struct GemmPlan { int cfg; int splits; int group_m; int sub = 0; int n_tail = 0; int active_cus = 0; };
 // allow_mf32: configurations with 32x32x16 MFMA tiles may be chosen (their
 // epilogues exist for the plain, residual-add and SwiGLU stores; SwiGLU needs
 // d_ffn % 32 == 0)
@@ -61,6 +64,12 @@ template <class Epi>
 hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M, int N,
                           int K, int splits, int group_m, int sub, int n_tail, const Epi& epi,
                           hipStream_t st);
+struct EpiLMHead;
+// LM head whose row count is known only on the device (epi.m_count): as many
+// blocks as fit on num_cu CUs, each XCD's blocks walking the tiles of its
+// contiguous range of column tiles whose rows lie below the count
+hipError_t gemm_dl_head_launch(int cfg, const bf16* A, int lda, const bf16* B, int ldb, int M,
+                               int N, int K, int num_cu, const EpiLMHead& epi, hipStream_t st);
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads);
 int gemm_dl_mfma(int cfg);
 int gemm_dl_subs(int cfg);
