@@ -188,7 +188,11 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // MHA QKV projection). The cheapest
 // (configuration, split) wins. 128x192 with two blocks per CU (cfg 22) runs
 // without K splits only (its table holds unsplit launches); the small tiles
-// only for few rows.
+// only for few rows. The eight-wave configurations that run the split-phase
+// tile form (6, 21, 29, 70) keep the tables measured for their two-ring form,
+// each entry scaled by the time ratio of the two forms measured at that
+// k-tile count in one run (full rounds: 0.94-0.98 for 6, 21 and 70, 0.87-0.94
+// for the three-stage 256x128 tile).
 namespace {
 struct RoundTable {
   int cfg, occ, max_m;
@@ -200,20 +204,17 @@ struct RoundTable {
 const RoundTable kRoundTables[] = {
     {6, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {24.8f, 30.1f, 36.3f, 51.8f, 48.5f, 58.8f, 75.5f, 85.9f, 89.7f, 106.1f, 130.4f, 151.4f, 227.9f, 279.8f, 430.1f}},
+     {24.3f, 28.9f, 34.4f, 49.2f, 46.2f, 55.8f, 71.9f, 82.2f, 85.6f, 101.6f, 124.3f, 143.9f, 216.3f, 267.3f, 405.0f}},
     {21, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {19.6f, 25.4f, 28.3f, 41.6f, 40.8f, 46.9f, 60.5f, 69.6f, 72.6f, 86.6f, 102.3f, 127.4f, 188.4f, 240.1f, 368.8f}},
+     {18.8f, 24.0f, 26.7f, 39.2f, 38.9f, 44.8f, 57.9f, 66.5f, 69.1f, 82.7f, 97.3f, 120.6f, 178.1f, 226.8f, 358.6f}},
     {22, 2, 1 << 30, true, 4, {56, 64, 192, 296}, {81.9f, 93.1f, 282.1f, 435.5f}},
     {29, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {15.9f, 18.6f, 22.8f, 31.9f, 31.3f, 37.1f, 46.3f, 54.8f, 58.0f, 71.1f, 81.9f, 99.7f, 147.8f, 193.6f, 284.2f}},
+     {15.0f, 17.4f, 21.1f, 28.6f, 28.0f, 33.1f, 42.1f, 49.4f, 52.3f, 64.4f, 73.5f, 89.4f, 131.1f, 171.4f, 246.3f}},
     {42, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
      {14.6f, 18.1f, 20.7f, 29.2f, 27.6f, 32.4f, 41.1f, 47.7f, 47.8f, 56.8f, 70.6f, 80.0f, 124.7f, 154.4f, 232.9f}},
-    {43, 1, 1 << 30, false, 15,
-     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {15.8f, 18.7f, 22.3f, 31.5f, 29.9f, 36.6f, 47.5f, 53.7f, 55.9f, 66.4f, 81.5f, 97.3f, 145.2f, 183.3f, 279.2f}},
     {1, 2, 128, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
      {17.1f, 22.4f, 25.6f, 37.3f, 33.5f, 40.8f, 51.1f, 65.7f, 65.8f, 71.1f, 90.8f, 119.1f, 171.0f, 214.9f, 335.1f}},
@@ -236,7 +237,7 @@ const RoundTable kRoundTables[] = {
     // a round takes 0.82-0.94 (mean 0.89) of a 256x256 round for 0.875 of its work
     {70, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {23.2f, 27.2f, 32.7f, 47.2f, 43.6f, 53.5f, 66.8f, 75.0f, 73.5f, 98.5f, 117.1f, 132.5f, 202.1f, 245.6f, 383.7f}},
+     {22.7f, 26.0f, 31.6f, 46.1f, 42.7f, 52.0f, 64.7f, 71.8f, 71.3f, 95.1f, 112.7f, 127.4f, 194.7f, 236.4f, 378.2f}},
 };
 
 double round_us(const RoundTable& t, double kt) {

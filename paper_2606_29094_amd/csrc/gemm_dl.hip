@@ -23,7 +23,8 @@ namespace dlm {
 
 // One BM x BN output tile at rows m0.., columns n0.., K range [kbeg, kend),
 // with the block's LDS at smem. tn and tz (column tile, K slice) are passed
-// to the K order and the epilogue.
+// to the K order and the epilogue. (Two-ring form; the split-phase form of
+// the eight-wave tiles follows.)
 template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, class Epi>
 __device__ __forceinline__ void dl_tile(char* smem, const bf16* __restrict__ A, int lda,
                                         const bf16* __restrict__ B, int ldb, int M, int N,
@@ -311,6 +312,230 @@ __device__ __forceinline__ void dl_tile(char* smem, const bf16* __restrict__ A, 
     epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
 }
 
+// wait until at most N vector-memory operations and no LDS operation of this
+// wave are in flight (gfx9 s_waitcnt: vmcnt in [3:0] and [15:14], lgkmcnt 0,
+// expcnt (7) not waited on)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+// Scheduling groups of a pipelined phase (masks 0x008: MFMA, 0x020: global
+// loads, 0x100: LDS reads): group I < NV + NR is one MFMA (while any of the
+// phase's P remain) followed by load I (I < NV) or fragment read I - NV; the
+// remaining MFMAs follow.
+template <int I, int NV, int NR, int P>
+__device__ __forceinline__ void sched_pipe() {
+  if constexpr (I < NV + NR) {
+    __builtin_amdgcn_sched_group_barrier(0x008, I < P ? 1 : 0, 0);
+    __builtin_amdgcn_sched_group_barrier(I < NV ? 0x020 : 0x100, 1, 0);
+    sched_pipe<I + 1, NV, NR, P>();
+  } else {
+    __builtin_amdgcn_sched_group_barrier(0x008, P > NV + NR ? P - NV - NR : 0, 0);
+  }
+}
+
+// Split-phase form for 64-deep k-tiles (128 bytes per row, 16x16x32 MFMAs,
+// two 32-wide k groups per k-tile), S stages each holding the A and the B
+// slice of one k-tile. The form above starts every k-tile by reading the
+// first group's fragments right after the barrier and waiting for them; here
+// the barrier sits in the middle of a k-tile instead: the MFMAs of group 0
+// run while group 1's fragments are read, then (once every wave's loads of
+// k-tile kt + 1 have landed and every wave has read all of k-tile kt) the
+// barrier, the load of k-tile kt + S into k-tile kt's stage, and the MFMAs of
+// group 1 while group 0 of k-tile kt + 1 is read. Both sides of the barrier
+// have MFMAs ready in registers. Same k order, same results bit for bit.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int S, class Epi>
+__device__ __forceinline__ void dls_tile(char* smem, const bf16* __restrict__ A, int lda,
+                                         const bf16* __restrict__ B, int ldb, int M, int N,
+                                         int m0, int n0, int tn, int tz, int kbeg, int kend,
+                                         const Epi& epi) {
+  static_assert(S >= 2 && S <= 4, "stages");
+  constexpr int RB = 128, BK = 64, CPR = 8, RPI = 8;
+  constexpr int NW = WAVES_M * WAVES_N;
+  constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
+  constexpr int FM = TM / 16, FN = TN / 16;
+  static_assert(FM * 16 == TM && FN * 16 == TN, "wave tile");
+  constexpr int STAGE = (BM + BN) * RB;   // A rows, then B rows
+  constexpr int NI_A = BM / RPI, NI_B = BN / RPI;
+  static_assert(NI_A * RPI == BM && NI_B * RPI == BN, "rows per instruction");
+  constexpr bool EVEN_A = NI_A % NW == 0, EVEN_B = NI_B % NW == 0;
+  constexpr int PERW_A = (NI_A + NW - 1) / NW, PERW_B = (NI_B + NW - 1) / NW;
+  constexpr int MINW = NI_A / NW + NI_B / NW;
+  constexpr int INFLIGHT = (S - 2) * MINW;
+  static_assert((S - 1) * MINW < 64, "vmcnt range");
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int nkt = kend > kbeg ? (kend - kbeg) / BK : 0;
+  const int krot = Epi::kRotateK && nkt > 0 ? tn % nkt : 0;
+  auto ktile = [&](int kt) { const int k = kt + krot; return k >= nkt ? k - nkt : k; };
+  auto swz = [](int r) { return r & 7; };
+  auto inst_a = [&](int j) { return EVEN_A ? wave * PERW_A + j : wave + j * NW; };
+  auto inst_b = [&](int j) { return EVEN_B ? wave * PERW_B + j : wave + j * NW; };
+  auto has_a = [&](int j) { return j < NI_A / NW || inst_a(j) < NI_A; };
+  auto has_b = [&](int j) { return j < NI_B / NW || inst_b(j) < NI_B; };
+  uint32_t srcA[PERW_A];
+  uint32_t srcB[PERW_B];
+#pragma unroll
+  for (int j = 0; j < PERW_A; ++j) {
+    const int row = RPI * inst_a(j) + lane / CPR;
+    const int cc = (lane % CPR) ^ swz(row);
+    srcA[j] = (uint32_t)min(m0 + row, M - 1) * (uint32_t)lda + kbeg + cc * 8;
+  }
+#pragma unroll
+  for (int j = 0; j < PERW_B; ++j) {
+    const int row = RPI * inst_b(j) + lane / CPR;
+    const int cc = (lane % CPR) ^ swz(row);
+    srcB[j] = (uint32_t)epi.b_row(min(n0 + row, N - 1)) * (uint32_t)ldb + kbeg + cc * 8;
+  }
+  // byte offsets (operands hold fewer than 2^31 bytes) from a wave-uniform
+  // base: the loads take the scalar-base form with one offset register each
+#pragma unroll
+  for (int j = 0; j < PERW_A; ++j) srcA[j] *= 2;
+#pragma unroll
+  for (int j = 0; j < PERW_B; ++j) srcB[j] *= 2;
+  auto issue = [&](int stage, int kt) {
+    char* dst = smem + stage * STAGE;
+    typedef __attribute__((address_space(1))) const char* gbytes;
+    const gbytes a = (gbytes)A + (size_t)kt * RB;
+    const gbytes b = (gbytes)B + (size_t)kt * RB;
+#pragma unroll
+    for (int j = 0; j < PERW_A; ++j)
+      if (has_a(j))
+        __builtin_amdgcn_global_load_lds((gptr_t)(a + srcA[j]),
+                                         (lptr_t)(dst + inst_a(j) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < PERW_B; ++j)
+      if (has_b(j))
+        __builtin_amdgcn_global_load_lds((gptr_t)(b + srcB[j]),
+                                         (lptr_t)(dst + BM * RB + inst_b(j) * 1024), 16, 0, 0);
+  };
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int a = 0; a < FM; ++a)
+#pragma unroll
+    for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // fragment rows: base + (lane & 15); group g's chunk 4 g + lane / 16 at slot chunk ^ (row & 7)
+  const int co0 = ((lane >> 4) ^ swz(lane & 15)) << 4;
+  const int co1 = ((4 + (lane >> 4)) ^ swz(lane & 15)) << 4;
+  const int a_off = (wm * TM + (lane & 15)) * RB;
+  const int b_off = BM * RB + (wn * TN + (lane & 15)) * RB;
+  u32x4 g0a[FM], g0b[FN], g1a[FM], g1b[FN];
+  auto read0 = [&](int stage) {
+    const char* p = smem + stage * STAGE;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+      g0a[fm] = *reinterpret_cast<const u32x4*>(p + a_off + fm * 16 * RB + co0);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+      g0b[fn] = *reinterpret_cast<const u32x4*>(p + b_off + fn * 16 * RB + co0);
+  };
+  auto read1 = [&](int stage) {
+    const char* p = smem + stage * STAGE;
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+      g1a[fm] = *reinterpret_cast<const u32x4*>(p + a_off + fm * 16 * RB + co1);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+      g1b[fn] = *reinterpret_cast<const u32x4*>(p + b_off + fn * 16 * RB + co1);
+  };
+  constexpr int NM = FM * FN, NR = FM + FN, NV = PERW_A + PERW_B;
+  auto mma0 = [&]() {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        acc[fm][fn] = mfma16_bf16(__builtin_bit_cast(bf16x8, g0a[fm]),
+                                  __builtin_bit_cast(bf16x8, g0b[fn]), acc[fm][fn]);
+  };
+  auto mma1 = [&]() {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        acc[fm][fn] = mfma16_bf16(__builtin_bit_cast(bf16x8, g1a[fm]),
+                                  __builtin_bit_cast(bf16x8, g1b[fn]), acc[fm][fn]);
+  };
+
+#pragma unroll
+  for (int j = 0; j < S; ++j)
+    if (j < nkt) issue(j, ktile(j));
+  if (nkt > 0) {
+    if (nkt >= S) wait_vmcnt<(S - 1) * MINW>(); else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    read0(0);
+  }
+  // group 0 of k-tile kt with the reads of its group 1
+  auto phase0 = [&](int st) {
+    read1(st);
+    mma0();
+    sched_pipe<0, 0, NR, NM>();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // steady state: the load of k-tile kt + S goes out with the MFMAs of
+  // group 1, and exactly the loads of k-tiles kt + 2 .. kt + S - 1 may stay
+  // in flight at the barrier
+  int kt = 0;
+  for (; kt + S < nkt; ++kt) {
+    const int st = kt % S;
+    phase0(st);
+    wait_vmcnt_lgkm0<INFLIGHT>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue(st, ktile(kt + S));
+    // group 1 of k-tile kt with the reads of group 0 of k-tile kt + 1
+    read0((kt + 1) % S);
+    mma1();
+    sched_pipe<0, NV, NR, NM>();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // the last k-tiles: nothing more to load, everything issued is waited for
+  for (; kt + 1 < nkt; ++kt) {
+    phase0(kt % S);
+    wait_vmcnt_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    read0((kt + 1) % S);
+    mma1();
+    sched_pipe<0, 0, NR, NM>();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (kt < nkt) {   // the last k-tile
+    phase0(kt % S);
+    mma1();
+  }
+  __syncthreads();
+  epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
+}
+
+// The tile form of a configuration: SA = 0 selects the split-phase form (SB
+// stages of A and B together), SA >= 2 the two-ring form.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, class Epi>
+__device__ __forceinline__ void any_tile(char* smem, const bf16* __restrict__ A, int lda,
+                                         const bf16* __restrict__ B, int ldb, int M, int N,
+                                         int m0, int n0, int tn, int tz, int kbeg, int kend,
+                                         const Epi& epi) {
+  if constexpr (SA == 0) {
+    static_assert(MF == 16, "split-phase form: 16x16x32 tiles");
+    dls_tile<BM, BN, WAVES_M, WAVES_N, SB, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn, tz, kbeg,
+                                                kend, epi);
+  } else {
+    dl_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn,
+                                                            tz, kbeg, kend, epi);
+  }
+}
+
+// LDS bytes of a configuration's block: SA = 0 (split-phase form) means SB
+// stages of A and B together
+constexpr int dl_lds_bytes(int BM, int BN, int SA, int SB, int RB) {
+  return SA == 0 ? SB * (BM + BN) * RB : (SA * BM + SB * BN) * RB;
+}
+
 // Sub-tiles of the last round: tile shapes a BM x BN tile splits into with the
 // same waves (halves: two (BM/2) x BN tiles; quarters: four (BM/2) x (BN/2)).
 template <int BM, int BN, int WAVES_M, int WAVES_N, int RB, int MF>
@@ -336,7 +561,7 @@ template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int 
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int k_per_split, int n_n, int n_m, int group_m, int n_tail, int sub, Epi epi) {
-  __shared__ __attribute__((aligned(1024))) char smem[(SA * BM + SB * BN) * RB];
+  __shared__ __attribute__((aligned(1024))) char smem[dl_lds_bytes(BM, BN, SA, SB, RB)];
   // Tile order. The logical order enumerates (K slice, row tile, column tile)
   // with the column tile fastest (group_m == 0), or, for weight matrices
   // larger than the last-level cache (group_m > 0), goes down a group of
@@ -401,7 +626,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   if (is_sub) {
     if constexpr (TAIL && Epi::kTailSplit && Sub::kQuarter) {
       if (sub == 4) {
-        dl_tile<BM / 2, BN / 2, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
+        any_tile<BM / 2, BN / 2, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
             smem, A, lda, B, ldb, M, N, m0 + (part >> 1) * (BM / 2), n0 + (part & 1) * (BN / 2),
             tn, tz, kbeg, kend, epi);
         return;
@@ -409,14 +634,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     }
     if constexpr (TAIL && Epi::kTailSplit && Sub::kHalf) {
       if (sub == 2) {
-        dl_tile<BM / 2, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
+        any_tile<BM / 2, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
             smem, A, lda, B, ldb, M, N, m0 + part * (BM / 2), n0, tn, tz, kbeg, kend, epi);
         return;
       }
     }
     return;   // not reached: the launcher only splits where the shapes allow
   }
-  dl_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn,
+  any_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn,
                                                           tz, kbeg, kend, epi);
 }
 
@@ -434,7 +659,7 @@ template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int 
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_head_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int n_n, EpiLMHead epi) {
-  __shared__ __attribute__((aligned(1024))) char smem[(SA * BM + SB * BN) * RB];
+  __shared__ __attribute__((aligned(1024))) char smem[dl_lds_bytes(BM, BN, SA, SB, RB)];
   const int rows = epi.m_count ? min(*epi.m_count, M) : M;
   const int act = rows > 0 ? (rows + BM - 1) / BM : 0;     // active row tiles
   const int xcd = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
@@ -444,29 +669,32 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_head_kernel(
   for (int a = k; a < total; a += nbx) {
     const int c = a / act;
     const int tn = c0 + c, tm = a - c * act;
-    dl_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, EpiLMHead>(
+    any_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, EpiLMHead>(
         smem, A, lda, B, ldb, M, N, tm * BM, tn * BN, tn, 0, 0, K, epi);
     __syncthreads();   // the epilogue's LDS reads before the next tile's loads
   }
 }
 
 // Tile configurations (BM, BN, waves M x N, activation stages, weight stages,
-// k-tile row bytes, MFMA tile 16x16x32 or 32x32x16). 256x224 (wave tiles of
-// 64x112, seven column fragments) covers a 3584-wide output in 16 column
-// tiles, so that 4096 rows make exactly one round of 256 tiles.
+// k-tile row bytes, MFMA tile 16x16x32 or 32x32x16). Activation stages 0: the
+// split-phase form with that many A+B stages (the eight-wave tiles, two
+// waves per SIMD: 3-10 % faster than the two-ring form of the same tile at
+// every k-tile count; the four-wave tiles, one wave per SIMD, run slower in
+// it and keep the two-ring form). 256x224 (wave tiles of 64x112, seven column
+// fragments) covers a 3584-wide output in 16 column tiles, so that 4096 rows
+// make exactly one round of 256 tiles.
 #define DL_CONFIGS(X)                   \
   X(1, 128, 128, 2, 2, 2, 2, 128, 16)   \
-  X(6, 256, 256, 2, 4, 2, 2, 128, 16)   \
+  X(6, 256, 256, 2, 4, 0, 2, 128, 16)   \
   X(10, 64, 128, 2, 2, 2, 2, 128, 16)   \
   X(11, 64, 128, 2, 2, 2, 3, 128, 16)   \
-  X(21, 256, 192, 4, 2, 2, 2, 128, 16)  \
+  X(21, 256, 192, 4, 2, 0, 2, 128, 16)  \
   X(22, 128, 192, 2, 2, 2, 2, 128, 16)  \
-  X(29, 256, 128, 4, 2, 2, 3, 128, 16)  \
+  X(29, 256, 128, 4, 2, 0, 3, 128, 16)  \
   X(42, 128, 192, 2, 2, 2, 3, 128, 16)  \
-  X(43, 256, 128, 4, 2, 2, 4, 128, 16)  \
   X(62, 256, 128, 2, 2, 2, 2, 128, 32)  \
   X(65, 384, 256, 4, 2, 2, 2, 128, 32)  \
-  X(70, 256, 224, 4, 2, 2, 2, 128, 16)
+  X(70, 256, 224, 4, 2, 0, 2, 128, 16)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
@@ -572,7 +800,7 @@ hipError_t gemm_dl_head_launch(int cfg, const bf16* A, int lda, const bf16* B, i
     if constexpr (MF_ == 32) return hipErrorInvalidValue;                                 \
     else {                                                                                \
       /* blocks per CU: bounded by the LDS (160 KB) and by 32 waves per CU */              \
-      constexpr int kLds = (SA_ * BM_ + S_ * BN_) * RB_, kWaves = WM_ * WN_;              \
+      constexpr int kLds = dl_lds_bytes(BM_, BN_, SA_, S_, RB_), kWaves = WM_ * WN_;              \
       constexpr int kOcc = 163840 / kLds < 32 / kWaves ? 163840 / kLds : 32 / kWaves;     \
       EpiLMHead e = epi;                                                                  \
       e.set_mfma(MF_);                                                                    \
