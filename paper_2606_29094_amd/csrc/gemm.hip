@@ -189,10 +189,12 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // (configuration, split) wins. 128x192 with two blocks per CU (cfg 22) runs
 // without K splits only (its table holds unsplit launches); the small tiles
 // only for few rows. The eight-wave configurations that run the split-phase
-// tile form (6, 21, 29, 70) keep the tables measured for their two-ring form,
+// tile form (6, 24, 29, 70) keep the tables measured for their two-ring form,
 // each entry scaled by the time ratio of the two forms measured at that
-// k-tile count in one run (full rounds: 0.94-0.98 for 6, 21 and 70, 0.87-0.94
-// for the three-stage 256x128 tile).
+// k-tile count in one run (full rounds: 0.94-0.98 for 6, 24 and 70); the
+// three-stage 256x128 tile (29) takes the mean of the estimates from the
+// tables of the two-ring 256x128 tiles it replaces (3- and 4-stage weight
+// rings, scaled by 0.87-0.94 and 0.90-0.97).
 namespace {
 struct RoundTable {
   int cfg, occ, max_m;
@@ -200,6 +202,7 @@ struct RoundTable {
   int n;
   float kt[15], us[15];
   int min_kt = 0;          // used only for at least this many k-tiles per block
+  int min_m = 0;           // used only for at least this many rows
 };
 const RoundTable kRoundTables[] = {
     {6, 1, 1 << 30, false, 15,
@@ -207,11 +210,18 @@ const RoundTable kRoundTables[] = {
      {24.3f, 28.9f, 34.4f, 49.2f, 46.2f, 55.8f, 71.9f, 82.2f, 85.6f, 101.6f, 124.3f, 143.9f, 216.3f, 267.3f, 405.0f}},
     {21, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {18.8f, 24.0f, 26.7f, 39.2f, 38.9f, 44.8f, 57.9f, 66.5f, 69.1f, 82.7f, 97.3f, 120.6f, 178.1f, 226.8f, 358.6f}},
+     {19.6f, 25.4f, 28.3f, 41.6f, 40.8f, 46.9f, 60.5f, 69.6f, 72.6f, 86.6f, 102.3f, 127.4f, 188.4f, 240.1f, 368.8f}},
+    // the split-phase form of 256x192 (cfg 24): faster than the two-ring form
+    // (cfg 21) once the weights are reused by several row tiles, ~3 % slower
+    // at 256-512 rows with every weight streamed once from HBM; its table is
+    // cfg 21's scaled by the measured time ratio of the two forms
+    {24, 1, 1 << 30, false, 15,
+     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
+     {18.8f, 24.0f, 26.7f, 39.2f, 38.9f, 44.8f, 57.9f, 66.5f, 69.1f, 82.7f, 97.3f, 120.6f, 178.1f, 226.8f, 358.6f}, 0, 1024},
     {22, 2, 1 << 30, true, 4, {56, 64, 192, 296}, {81.9f, 93.1f, 282.1f, 435.5f}},
     {29, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {15.0f, 17.4f, 21.1f, 28.6f, 28.0f, 33.1f, 42.1f, 49.4f, 52.3f, 64.4f, 73.5f, 89.4f, 131.1f, 171.4f, 246.3f}},
+     {15.2f, 17.6f, 21.0f, 28.5f, 27.5f, 33.1f, 42.6f, 49.1f, 51.6f, 63.0f, 74.3f, 89.6f, 131.7f, 168.7f, 249.4f}},
     {42, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
      {14.6f, 18.1f, 20.7f, 29.2f, 27.6f, 32.4f, 41.1f, 47.7f, 47.8f, 56.8f, 70.6f, 80.0f, 124.7f, 154.4f, 232.9f}},
@@ -268,7 +278,7 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu, boo
   }
   double best_t = 1e30;
   for (const RoundTable& c : kRoundTables) {
-    if (M > c.max_m) continue;
+    if (M > c.max_m || M < c.min_m) continue;
     if (!allow_mf32 && gemm_dl_mfma(c.cfg) == 32) continue;
     if (!allow_odd && gemm_dl_odd(c.cfg)) continue;
     int bm, bn, th;

@@ -688,7 +688,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_head_kernel(
   X(6, 256, 256, 2, 4, 0, 2, 128, 16)   \
   X(10, 64, 128, 2, 2, 2, 2, 128, 16)   \
   X(11, 64, 128, 2, 2, 2, 3, 128, 16)   \
-  X(21, 256, 192, 4, 2, 0, 2, 128, 16)  \
+  X(21, 256, 192, 4, 2, 2, 2, 128, 16)  \
+  X(24, 256, 192, 4, 2, 0, 2, 128, 16)  \
   X(22, 128, 192, 2, 2, 2, 2, 128, 16)  \
   X(29, 256, 128, 4, 2, 0, 3, 128, 16)  \
   X(42, 128, 192, 2, 2, 2, 3, 128, 16)  \

@@ -838,7 +838,7 @@ dlm_status dlm_debug_gemm(int32_t cfg, int32_t epilogue, int32_t sub, int32_t n_
     return fail(DLM_EINVAL, "configuration %d has no SwiGLU epilogue (odd fragment count)", cfg);
   if (sub != 0 && ((sub != 2 && sub != 4) || !(gemm_dl_subs(cfg) & sub)))
     return fail(DLM_EINVAL, "configuration %d has no %d-way sub-tiles", cfg, sub);
-  if (sub != 0 && (long)n_tail > (long)ceil_div(M, tm) * ceil_div(N, tn))
+  if (sub != 0 && (long)n_tail > (long)ceil_div(M, tm) * ceil_div(N, tn) * splits)
     return fail(DLM_EINVAL, "n_tail %d beyond the tile count", n_tail);
   const hipError_t e = gemm_debug_launch(cfg, epilogue, sub, n_tail, group_m, splits,
                                          reinterpret_cast<const bf16*>(a),
