@@ -188,13 +188,16 @@ static hipError_t launch(const GemmPlan& p, const T* A, int lda, const T* B, int
 // MHA QKV projection). The cheapest
 // (configuration, split) wins. 128x192 with two blocks per CU (cfg 22) runs
 // without K splits only (its table holds unsplit launches); the small tiles
-// only for few rows. The eight-wave configurations that run the split-phase
-// tile form (6, 24, 29, 70) keep the tables measured for their two-ring form,
-// each entry scaled by the time ratio of the two forms measured at that
-// k-tile count in one run (full rounds: 0.94-0.98 for 6, 24 and 70); the
-// three-stage 256x128 tile (29) takes the mean of the estimates from the
-// tables of the two-ring 256x128 tiles it replaces (3- and 4-stage weight
-// rings, scaled by 0.87-0.94 and 0.90-0.97).
+// only for few rows. The eight-wave configurations run the split-phase tile
+// form with a three-stage weight ring (6, 21, 70) or three stages of both
+// operands (29); their tables are the ones measured for their two-ring form,
+// each entry scaled by the time ratios of the forms measured at that k-tile
+// count (full rounds: 0.94-0.98 from the split-phase loop, about 0.98-0.99
+// more from the third weight stage; the 256x192 tile 0.93, measured at 256 to
+// 6400 rows with the weights streamed from HBM); the three-stage 256x128 tile
+// (29) takes the mean of the estimates from the tables of the two-ring
+// 256x128 tiles it replaces (3- and 4-stage weight rings, scaled by
+// 0.87-0.94 and 0.90-0.97).
 namespace {
 struct RoundTable {
   int cfg, occ, max_m;
@@ -202,22 +205,14 @@ struct RoundTable {
   int n;
   float kt[15], us[15];
   int min_kt = 0;          // used only for at least this many k-tiles per block
-  int min_m = 0;           // used only for at least this many rows
 };
 const RoundTable kRoundTables[] = {
     {6, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {24.3f, 28.9f, 34.4f, 49.2f, 46.2f, 55.8f, 71.9f, 82.2f, 85.6f, 101.6f, 124.3f, 143.9f, 216.3f, 267.3f, 405.0f}},
+     {23.9f, 28.5f, 33.9f, 48.5f, 45.5f, 55.0f, 70.8f, 81.0f, 84.3f, 100.1f, 122.4f, 141.7f, 213.1f, 263.3f, 398.9f}},
     {21, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {19.6f, 25.4f, 28.3f, 41.6f, 40.8f, 46.9f, 60.5f, 69.6f, 72.6f, 86.6f, 102.3f, 127.4f, 188.4f, 240.1f, 368.8f}},
-    // the split-phase form of 256x192 (cfg 24): faster than the two-ring form
-    // (cfg 21) once the weights are reused by several row tiles, ~3 % slower
-    // at 256-512 rows with every weight streamed once from HBM; its table is
-    // cfg 21's scaled by the measured time ratio of the two forms
-    {24, 1, 1 << 30, false, 15,
-     {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {18.8f, 24.0f, 26.7f, 39.2f, 38.9f, 44.8f, 57.9f, 66.5f, 69.1f, 82.7f, 97.3f, 120.6f, 178.1f, 226.8f, 358.6f}, 0, 1024},
+     {18.2f, 23.6f, 26.3f, 38.7f, 37.9f, 43.6f, 56.3f, 64.7f, 67.5f, 80.5f, 95.1f, 118.5f, 175.2f, 223.3f, 343.0f}},
     {22, 2, 1 << 30, true, 4, {56, 64, 192, 296}, {81.9f, 93.1f, 282.1f, 435.5f}},
     {29, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
@@ -247,7 +242,7 @@ const RoundTable kRoundTables[] = {
     // a round takes 0.82-0.94 (mean 0.89) of a 256x256 round for 0.875 of its work
     {70, 1, 1 << 30, false, 15,
      {8, 14, 16, 24, 28, 32, 37, 48, 56, 64, 74, 96, 148, 192, 296},
-     {22.7f, 26.0f, 31.6f, 46.1f, 42.7f, 52.0f, 64.7f, 71.8f, 71.3f, 95.1f, 112.7f, 127.4f, 194.7f, 236.4f, 378.2f}},
+     {22.5f, 25.7f, 31.3f, 45.6f, 42.3f, 51.5f, 64.1f, 71.1f, 70.6f, 94.1f, 111.6f, 126.1f, 192.8f, 234.0f, 374.4f}},
 };
 
 double round_us(const RoundTable& t, double kt) {
@@ -278,7 +273,7 @@ GemmPlan gemm_plan(int es, int M, int N, int K, bool splittable, int num_cu, boo
   }
   double best_t = 1e30;
   for (const RoundTable& c : kRoundTables) {
-    if (M > c.max_m || M < c.min_m) continue;
+    if (M > c.max_m) continue;
     if (!allow_mf32 && gemm_dl_mfma(c.cfg) == 32) continue;
     if (!allow_odd && gemm_dl_odd(c.cfg)) continue;
     int bm, bn, th;

@@ -337,34 +337,45 @@ __device__ __forceinline__ void sched_pipe() {
 }
 
 // Split-phase form for 64-deep k-tiles (128 bytes per row, 16x16x32 MFMAs,
-// two 32-wide k groups per k-tile), S stages each holding the A and the B
-// slice of one k-tile. The form above starts every k-tile by reading the
-// first group's fragments right after the barrier and waiting for them; here
-// the barrier sits in the middle of a k-tile instead: the MFMAs of group 0
-// run while group 1's fragments are read, then (once every wave's loads of
-// k-tile kt + 1 have landed and every wave has read all of k-tile kt) the
-// barrier, the load of k-tile kt + S into k-tile kt's stage, and the MFMAs of
-// group 1 while group 0 of k-tile kt + 1 is read. Both sides of the barrier
-// have MFMAs ready in registers. Same k order, same results bit for bit.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int S, class Epi>
+// two 32-wide k groups per k-tile), with an SA-stage activation ring and an
+// SB-stage weight ring (SB >= SA). The two-ring form above starts every
+// k-tile by reading the first group's fragments right after the barrier and
+// waiting for them; here the barrier sits in the middle of a k-tile instead:
+// the MFMAs of group 0 run while group 1's fragments are read, then (once
+// this wave's loads of k-tile kt + 1 have landed and it has read all of
+// k-tile kt; the barrier makes that hold for every wave) the barrier, the
+// loads of A(kt + SA) and B(kt + SB) into k-tile kt's stages, and the MFMAs
+// of group 1 while group 0 of k-tile kt + 1 is read. Both sides of the
+// barrier have MFMAs ready in registers. Same k order, same results bit for
+// bit.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, class Epi>
 __device__ __forceinline__ void dls_tile(char* smem, const bf16* __restrict__ A, int lda,
                                          const bf16* __restrict__ B, int ldb, int M, int N,
                                          int m0, int n0, int tn, int tz, int kbeg, int kend,
                                          const Epi& epi) {
-  static_assert(S >= 2 && S <= 4, "stages");
+  static_assert(SA >= 2 && SB >= SA && SB <= 4, "stages");
   constexpr int RB = 128, BK = 64, CPR = 8, RPI = 8;
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
   constexpr int FM = TM / 16, FN = TN / 16;
   static_assert(FM * 16 == TM && FN * 16 == TN, "wave tile");
-  constexpr int STAGE = (BM + BN) * RB;   // A rows, then B rows
+  constexpr int STAGE_A = BM * RB, STAGE_B = BN * RB;
   constexpr int NI_A = BM / RPI, NI_B = BN / RPI;
   static_assert(NI_A * RPI == BM && NI_B * RPI == BN, "rows per instruction");
   constexpr bool EVEN_A = NI_A % NW == 0, EVEN_B = NI_B % NW == 0;
   constexpr int PERW_A = (NI_A + NW - 1) / NW, PERW_B = (NI_B + NW - 1) / NW;
-  constexpr int MINW = NI_A / NW + NI_B / NW;
-  constexpr int INFLIGHT = (S - 2) * MINW;
-  static_assert((S - 1) * MINW < 64, "vmcnt range");
+  constexpr int MINW_A = NI_A / NW, MINW_B = NI_B / NW;
+  // Issue order: the prologue loads A0 B0 A1 B1 .. A(SA-1) B(SA-1), then
+  // B(SA) .. B(SB-1); iteration j loads A(j + SA) then B(j + SB). At the
+  // barrier of iteration kt the loads that may stay in flight are those
+  // issued after the later of A(kt + 1) and B(kt + 1), counted for the waves
+  // with the fewest loads (a wave with more then also waits for a load or
+  // two of a later k-tile, which is safe).
+  constexpr int INFLIGHT = SA < SB ? MINW_B + (SA - 2) * (MINW_A + MINW_B)
+                                   : (SA - 2) * (MINW_A + MINW_B);
+  constexpr int PROLOGUE = (SA - 1) * MINW_A + (SB - 1) * MINW_B;   // after A0, B0
+  static_assert(PROLOGUE < 64, "vmcnt range");
+  char* const smem_b = smem + SA * STAGE_A;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -374,8 +385,8 @@ __device__ __forceinline__ void dls_tile(char* smem, const bf16* __restrict__ A,
   auto swz = [](int r) { return r & 7; };
   auto inst_a = [&](int j) { return EVEN_A ? wave * PERW_A + j : wave + j * NW; };
   auto inst_b = [&](int j) { return EVEN_B ? wave * PERW_B + j : wave + j * NW; };
-  auto has_a = [&](int j) { return j < NI_A / NW || inst_a(j) < NI_A; };
-  auto has_b = [&](int j) { return j < NI_B / NW || inst_b(j) < NI_B; };
+  auto has_a = [&](int j) { return j < MINW_A || inst_a(j) < NI_A; };
+  auto has_b = [&](int j) { return j < MINW_B || inst_b(j) < NI_B; };
   uint32_t srcA[PERW_A];
   uint32_t srcB[PERW_B];
 #pragma unroll
@@ -390,27 +401,23 @@ __device__ __forceinline__ void dls_tile(char* smem, const bf16* __restrict__ A,
     const int cc = (lane % CPR) ^ swz(row);
     srcB[j] = (uint32_t)epi.b_row(min(n0 + row, N - 1)) * (uint32_t)ldb + kbeg + cc * 8;
   }
-  // byte offsets (operands hold fewer than 2^31 bytes) from a wave-uniform
-  // base: the loads take the scalar-base form with one offset register each
-#pragma unroll
-  for (int j = 0; j < PERW_A; ++j) srcA[j] *= 2;
-#pragma unroll
-  for (int j = 0; j < PERW_B; ++j) srcB[j] *= 2;
-  auto issue = [&](int stage, int kt) {
-    char* dst = smem + stage * STAGE;
-    typedef __attribute__((address_space(1))) const char* gbytes;
-    const gbytes a = (gbytes)A + (size_t)kt * RB;
-    const gbytes b = (gbytes)B + (size_t)kt * RB;
+  auto issue_a = [&](int stage, int kt) {
+    char* dst = smem + stage * STAGE_A;
+    const bf16* a = A + kt * BK;
 #pragma unroll
     for (int j = 0; j < PERW_A; ++j)
       if (has_a(j))
         __builtin_amdgcn_global_load_lds((gptr_t)(a + srcA[j]),
                                          (lptr_t)(dst + inst_a(j) * 1024), 16, 0, 0);
+  };
+  auto issue_b = [&](int stage, int kt) {
+    char* dst = smem_b + stage * STAGE_B;
+    const bf16* b = B + kt * BK;
 #pragma unroll
     for (int j = 0; j < PERW_B; ++j)
       if (has_b(j))
         __builtin_amdgcn_global_load_lds((gptr_t)(b + srcB[j]),
-                                         (lptr_t)(dst + BM * RB + inst_b(j) * 1024), 16, 0, 0);
+                                         (lptr_t)(dst + inst_b(j) * 1024), 16, 0, 0);
   };
 
   f32x4 acc[FM][FN];
@@ -423,25 +430,27 @@ __device__ __forceinline__ void dls_tile(char* smem, const bf16* __restrict__ A,
   const int co0 = ((lane >> 4) ^ swz(lane & 15)) << 4;
   const int co1 = ((4 + (lane >> 4)) ^ swz(lane & 15)) << 4;
   const int a_off = (wm * TM + (lane & 15)) * RB;
-  const int b_off = BM * RB + (wn * TN + (lane & 15)) * RB;
+  const int b_off = (wn * TN + (lane & 15)) * RB;
   u32x4 g0a[FM], g0b[FN], g1a[FM], g1b[FN];
-  auto read0 = [&](int stage) {
-    const char* p = smem + stage * STAGE;
+  auto read0 = [&](int sa, int sb) {
+    const char* pa = smem + sa * STAGE_A;
+    const char* pb = smem_b + sb * STAGE_B;
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
-      g0a[fm] = *reinterpret_cast<const u32x4*>(p + a_off + fm * 16 * RB + co0);
+      g0a[fm] = *reinterpret_cast<const u32x4*>(pa + a_off + fm * 16 * RB + co0);
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn)
-      g0b[fn] = *reinterpret_cast<const u32x4*>(p + b_off + fn * 16 * RB + co0);
+      g0b[fn] = *reinterpret_cast<const u32x4*>(pb + b_off + fn * 16 * RB + co0);
   };
-  auto read1 = [&](int stage) {
-    const char* p = smem + stage * STAGE;
+  auto read1 = [&](int sa, int sb) {
+    const char* pa = smem + sa * STAGE_A;
+    const char* pb = smem_b + sb * STAGE_B;
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
-      g1a[fm] = *reinterpret_cast<const u32x4*>(p + a_off + fm * 16 * RB + co1);
+      g1a[fm] = *reinterpret_cast<const u32x4*>(pa + a_off + fm * 16 * RB + co1);
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn)
-      g1b[fn] = *reinterpret_cast<const u32x4*>(p + b_off + fn * 16 * RB + co1);
+      g1b[fn] = *reinterpret_cast<const u32x4*>(pb + b_off + fn * 16 * RB + co1);
   };
   constexpr int NM = FM * FN, NR = FM + FN, NV = PERW_A + PERW_B;
   auto mma0 = [&]() {
@@ -462,78 +471,76 @@ __device__ __forceinline__ void dls_tile(char* smem, const bf16* __restrict__ A,
   };
 
 #pragma unroll
-  for (int j = 0; j < S; ++j)
-    if (j < nkt) issue(j, ktile(j));
+  for (int j = 0; j < SB; ++j) {
+    if (j < SA && j < nkt) issue_a(j, ktile(j));
+    if (j < nkt) issue_b(j, ktile(j));
+  }
   if (nkt > 0) {
-    if (nkt >= S) wait_vmcnt<(S - 1) * MINW>(); else wait_vmcnt<0>();
+    if (nkt >= SB) wait_vmcnt<PROLOGUE>(); else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    read0(0);
+    read0(0, 0);
   }
   // group 0 of k-tile kt with the reads of its group 1
-  auto phase0 = [&](int st) {
-    read1(st);
+  auto phase0 = [&](int kt) {
+    read1(kt % SA, kt % SB);
     mma0();
     sched_pipe<0, 0, NR, NM>();
     __builtin_amdgcn_sched_barrier(0);
   };
-  // steady state: the load of k-tile kt + S goes out with the MFMAs of
-  // group 1, and exactly the loads of k-tiles kt + 2 .. kt + S - 1 may stay
-  // in flight at the barrier
+  // steady state: the loads of k-tiles kt + SA (A) and kt + SB (B) go out
+  // with the MFMAs of group 1
   int kt = 0;
-  for (; kt + S < nkt; ++kt) {
-    const int st = kt % S;
-    phase0(st);
+  for (; kt + SB < nkt; ++kt) {
+    phase0(kt);
     wait_vmcnt_lgkm0<INFLIGHT>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    issue(st, ktile(kt + S));
+    issue_a(kt % SA, ktile(kt + SA));
+    issue_b(kt % SB, ktile(kt + SB));
     // group 1 of k-tile kt with the reads of group 0 of k-tile kt + 1
-    read0((kt + 1) % S);
+    read0((kt + 1) % SA, (kt + 1) % SB);
     mma1();
     sched_pipe<0, NV, NR, NM>();
     __builtin_amdgcn_sched_barrier(0);
   }
-  // the last k-tiles: nothing more to load, everything issued is waited for
+  // the last k-tiles: the remaining activation loads, everything issued is
+  // waited for
   for (; kt + 1 < nkt; ++kt) {
-    phase0(kt % S);
+    phase0(kt);
     wait_vmcnt_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    read0((kt + 1) % S);
+    if (kt + SA < nkt) issue_a(kt % SA, ktile(kt + SA));
+    read0((kt + 1) % SA, (kt + 1) % SB);
     mma1();
     sched_pipe<0, 0, NR, NM>();
     __builtin_amdgcn_sched_barrier(0);
   }
   if (kt < nkt) {   // the last k-tile
-    phase0(kt % S);
+    phase0(kt);
     mma1();
   }
   __syncthreads();
   epi(acc, m0 + wm * TM, n0 + wn * TN, lane, wn, smem, WAVES_N, BM, m0, tn, tz);
 }
 
-// The tile form of a configuration: SA = 0 selects the split-phase form (SB
-// stages of A and B together), SA >= 2 the two-ring form.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, class Epi>
+// The tile form of a configuration: SP = 1 the split-phase form, SP = 0 the
+// two-ring form (both with SA activation and SB weight stages).
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, int SP,
+          class Epi>
 __device__ __forceinline__ void any_tile(char* smem, const bf16* __restrict__ A, int lda,
                                          const bf16* __restrict__ B, int ldb, int M, int N,
                                          int m0, int n0, int tn, int tz, int kbeg, int kend,
                                          const Epi& epi) {
-  if constexpr (SA == 0) {
-    static_assert(MF == 16, "split-phase form: 16x16x32 tiles");
-    dls_tile<BM, BN, WAVES_M, WAVES_N, SB, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn, tz, kbeg,
-                                                kend, epi);
+  if constexpr (SP) {
+    static_assert(MF == 16 && RB == 128, "split-phase form: 16x16x32 tiles, 128-byte rows");
+    dls_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn, tz,
+                                                    kbeg, kend, epi);
   } else {
     dl_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn,
                                                             tz, kbeg, kend, epi);
   }
-}
-
-// LDS bytes of a configuration's block: SA = 0 (split-phase form) means SB
-// stages of A and B together
-constexpr int dl_lds_bytes(int BM, int BN, int SA, int SB, int RB) {
-  return SA == 0 ? SB * (BM + BN) * RB : (SA * BM + SB * BN) * RB;
 }
 
 // Sub-tiles of the last round: tile shapes a BM x BN tile splits into with the
@@ -556,12 +563,12 @@ struct SubTiles {
 // that fills at most half of the CUs, its tiles then finish in a fraction of a
 // whole tile's time. Sub-tiles accumulate every output element over the same
 // k order as whole tiles, so the results are the same bit for bit.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, bool TAIL,
-          class Epi>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, int SP,
+          bool TAIL, class Epi>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int k_per_split, int n_n, int n_m, int group_m, int n_tail, int sub, Epi epi) {
-  __shared__ __attribute__((aligned(1024))) char smem[dl_lds_bytes(BM, BN, SA, SB, RB)];
+  __shared__ __attribute__((aligned(1024))) char smem[(SA * BM + SB * BN) * RB];
   // Tile order. The logical order enumerates (K slice, row tile, column tile)
   // with the column tile fastest (group_m == 0), or, for weight matrices
   // larger than the last-level cache (group_m > 0), goes down a group of
@@ -626,7 +633,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
   if (is_sub) {
     if constexpr (TAIL && Epi::kTailSplit && Sub::kQuarter) {
       if (sub == 4) {
-        any_tile<BM / 2, BN / 2, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
+        any_tile<BM / 2, BN / 2, WAVES_M, WAVES_N, SA, SB, RB, MF, SP, Epi>(
             smem, A, lda, B, ldb, M, N, m0 + (part >> 1) * (BM / 2), n0 + (part & 1) * (BN / 2),
             tn, tz, kbeg, kend, epi);
         return;
@@ -634,14 +641,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
     }
     if constexpr (TAIL && Epi::kTailSplit && Sub::kHalf) {
       if (sub == 2) {
-        any_tile<BM / 2, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(
+        any_tile<BM / 2, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, SP, Epi>(
             smem, A, lda, B, ldb, M, N, m0 + part * (BM / 2), n0, tn, tz, kbeg, kend, epi);
         return;
       }
     }
     return;   // not reached: the launcher only splits where the shapes allow
   }
-  any_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn,
+  any_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, SP, Epi>(smem, A, lda, B, ldb, M, N, m0, n0, tn,
                                                           tz, kbeg, kend, epi);
 }
 
@@ -655,11 +662,11 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_kernel(
 // of column tiles, the rows of one column tile on consecutive blocks, so
 // those share the column's weight tile in L2 at about the same time, as in
 // the grouped order. No block waits on another.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int SA, int SB, int RB, int MF, int SP>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_head_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ B, int ldb, int M, int N,
     int K, int n_n, EpiLMHead epi) {
-  __shared__ __attribute__((aligned(1024))) char smem[dl_lds_bytes(BM, BN, SA, SB, RB)];
+  __shared__ __attribute__((aligned(1024))) char smem[(SA * BM + SB * BN) * RB];
   const int rows = epi.m_count ? min(*epi.m_count, M) : M;
   const int act = rows > 0 ? (rows + BM - 1) / BM : 0;     // active row tiles
   const int xcd = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
@@ -669,37 +676,36 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void gemm_dl_head_kernel(
   for (int a = k; a < total; a += nbx) {
     const int c = a / act;
     const int tn = c0 + c, tm = a - c * act;
-    any_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, EpiLMHead>(
+    any_tile<BM, BN, WAVES_M, WAVES_N, SA, SB, RB, MF, SP, EpiLMHead>(
         smem, A, lda, B, ldb, M, N, tm * BM, tn * BN, tn, 0, 0, K, epi);
     __syncthreads();   // the epilogue's LDS reads before the next tile's loads
   }
 }
 
 // Tile configurations (BM, BN, waves M x N, activation stages, weight stages,
-// k-tile row bytes, MFMA tile 16x16x32 or 32x32x16). Activation stages 0: the
-// split-phase form with that many A+B stages (the eight-wave tiles, two
-// waves per SIMD: 3-10 % faster than the two-ring form of the same tile at
-// every k-tile count; the four-wave tiles, one wave per SIMD, run slower in
-// it and keep the two-ring form). 256x224 (wave tiles of 64x112, seven column
+// k-tile row bytes, MFMA tile 16x16x32 or 32x32x16, split-phase form). The
+// split-phase form serves the eight-wave tiles (two waves per SIMD: 3-10 %
+// faster than the two-ring form of the same tile at every k-tile count; the
+// four-wave tiles, one wave per SIMD, run slower in it and keep the two-ring
+// form). 256x224 (wave tiles of 64x112, seven column
 // fragments) covers a 3584-wide output in 16 column tiles, so that 4096 rows
 // make exactly one round of 256 tiles.
-#define DL_CONFIGS(X)                   \
-  X(1, 128, 128, 2, 2, 2, 2, 128, 16)   \
-  X(6, 256, 256, 2, 4, 0, 2, 128, 16)   \
-  X(10, 64, 128, 2, 2, 2, 2, 128, 16)   \
-  X(11, 64, 128, 2, 2, 2, 3, 128, 16)   \
-  X(21, 256, 192, 4, 2, 2, 2, 128, 16)  \
-  X(24, 256, 192, 4, 2, 0, 2, 128, 16)  \
-  X(22, 128, 192, 2, 2, 2, 2, 128, 16)  \
-  X(29, 256, 128, 4, 2, 0, 3, 128, 16)  \
-  X(42, 128, 192, 2, 2, 2, 3, 128, 16)  \
-  X(62, 256, 128, 2, 2, 2, 2, 128, 32)  \
-  X(65, 384, 256, 4, 2, 2, 2, 128, 32)  \
-  X(70, 256, 224, 4, 2, 0, 2, 128, 16)
+#define DL_CONFIGS(X)                      \
+  X(1, 128, 128, 2, 2, 2, 2, 128, 16, 0)   \
+  X(6, 256, 256, 2, 4, 2, 3, 128, 16, 1)   \
+  X(10, 64, 128, 2, 2, 2, 2, 128, 16, 0)   \
+  X(11, 64, 128, 2, 2, 2, 3, 128, 16, 0)   \
+  X(21, 256, 192, 4, 2, 2, 3, 128, 16, 1)  \
+  X(22, 128, 192, 2, 2, 2, 2, 128, 16, 0)  \
+  X(29, 256, 128, 4, 2, 3, 3, 128, 16, 1)  \
+  X(42, 128, 192, 2, 2, 2, 3, 128, 16, 0)  \
+  X(62, 256, 128, 2, 2, 2, 2, 128, 32, 0)  \
+  X(65, 384, 256, 4, 2, 2, 2, 128, 32, 0)  \
+  X(70, 256, 224, 4, 2, 2, 3, 128, 16, 1)
 
 int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_) \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_) \
   case id: *bm = BM_; *bn = BN_; *threads = WM_ * WN_ * 64; return 1;
     DL_CONFIGS(X)
 #undef X
@@ -709,7 +715,7 @@ int gemm_dl_tile(int cfg, int* bm, int* bn, int* threads) {
 
 int gemm_dl_mfma(int cfg) {
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_) \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_) \
   case id: return MF_;
     DL_CONFIGS(X)
 #undef X
@@ -721,7 +727,7 @@ int gemm_dl_mfma(int cfg) {
 // SwiGLU epilogue, which stores gate/up fragment pairs, cannot run it).
 int gemm_dl_odd(int cfg) {
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_) \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_) \
   case id: return (BN_ / WN_ / MF_) % 2;
     DL_CONFIGS(X)
 #undef X
@@ -733,7 +739,7 @@ int gemm_dl_odd(int cfg) {
 // bit 2: quarters).
 int gemm_dl_subs(int cfg) {
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                          \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_)                          \
   case id: {                                                                \
     typedef SubTiles<BM_, BN_, WM_, WN_, RB_, MF_> S;                       \
     return (S::kHalf ? 2 : 0) | (S::kQuarter ? 4 : 0);                      \
@@ -758,7 +764,7 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
   if (n_tail < 0 || (sub != 0 && (!Epi::kTailSplit || !(gemm_dl_subs(cfg) & sub))))
     return hipErrorInvalidValue;
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                                        \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_)                                        \
   case id: {                                                                             \
     if constexpr ((MF_ == 32 && !Epi::kMf32) ||                                          \
                   (!Epi::kOddFragments && (BN_ / WN_ / MF_) % 2 != 0))                   \
@@ -772,11 +778,11 @@ hipError_t gemm_dl_launch(int cfg, const bf16* A, int lda, const bf16* B, int ld
       Epi e = epi;                                                                       \
       e.set_mfma(MF_);                                                                   \
       if (n_tail == 0) {                                                                 \
-        DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, false, Epi>),   \
+        DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_, false, Epi>),   \
                    dim3(n_n, n_m, splits), dim3(WM_ * WN_ * 64), 0, st, A, lda, B, ldb, M, \
                    N, K, kps, n_n, n_m, group_m, 0, 0, e);                               \
       } else if constexpr (Epi::kTailSplit) {                                            \
-        DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, true, Epi>),    \
+        DLM_LAUNCH((gemm_dl_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_, true, Epi>),    \
                    dim3((unsigned)blocks), dim3(WM_ * WN_ * 64), 0, st, A, lda, B, ldb, M, \
                    N, K, kps, n_n, n_m, group_m, n_tail, sub, e);                        \
       }                                                                                  \
@@ -796,16 +802,16 @@ hipError_t gemm_dl_head_launch(int cfg, const bf16* A, int lda, const bf16* B, i
   if ((double)(M - 1) * lda + K >= 4294967296.0 || (double)(N - 1) * ldb + K >= 4294967296.0)
     return hipErrorInvalidValue;
   switch (cfg) {
-#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_)                                         \
+#define X(id, BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_)                                         \
   case id: {                                                                              \
     if constexpr (MF_ == 32) return hipErrorInvalidValue;                                 \
     else {                                                                                \
       /* blocks per CU: bounded by the LDS (160 KB) and by 32 waves per CU */              \
-      constexpr int kLds = dl_lds_bytes(BM_, BN_, SA_, S_, RB_), kWaves = WM_ * WN_;              \
+      constexpr int kLds = (SA_ * BM_ + S_ * BN_) * RB_, kWaves = WM_ * WN_;                     \
       constexpr int kOcc = 163840 / kLds < 32 / kWaves ? 163840 / kLds : 32 / kWaves;     \
       EpiLMHead e = epi;                                                                  \
       e.set_mfma(MF_);                                                                    \
-      DLM_LAUNCH((gemm_dl_head_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_>),            \
+      DLM_LAUNCH((gemm_dl_head_kernel<BM_, BN_, WM_, WN_, SA_, S_, RB_, MF_, SP_>),            \
                  dim3(num_cu * (kOcc > 0 ? kOcc : 1)), dim3(kWaves * 64), 0, st, A, lda, B, \
                  ldb, M, N, K, ceil_div(N, BN_), e);                                      \
       return hipGetLastError();                                                           \
