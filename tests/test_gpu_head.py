@@ -41,8 +41,10 @@ def test_head_confidence_matches_oracle(gpu, cfg, inv_tau):
     W = t["lm_head"].float().cpu().numpy()
     rng = np.random.default_rng(7)
     dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-    # 300 rows: two row tiles (the launch whose blocks walk the active tiles)
-    for M in (1, 37, 256) + ((300,) if cfg.dtype == "bf16" else ()):
+    # 300 and 400 rows: several row tiles (the launch whose blocks walk the
+    # active tiles), with 128x192 two-ring tiles at 300 rows and 256x256
+    # split-phase tiles at 400 (a ragged second row tile)
+    for M in (1, 37, 256) + ((300, 400) if cfg.dtype == "bf16" else ()):
         u = torch.from_numpy(rng.standard_normal((M, cfg.d_model)).astype(np.float32)).to(dt)
         u[0] = 0                                   # closed form: 1/V, token 0
         if M > 1:
