@@ -66,17 +66,17 @@ def measured_traffic(kernel_class: str, workload: str):
     return float(t["hbm_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
 
-def step_rows(reqs, mode):
-    """(recomputed rows, keys) of each request for the step about to run."""
+def launched_rows(dreqs, mode, refresh_flag):
+    """(recomputed rows, keys) of each request of a step already enqueued,
+    from its request descriptors (refresh_flag: the descriptor's recompute bit)."""
     out = []
-    for r in reqs:
-        s = r.block_start
-        if mode == "none" or r.refreshed_block != s:
-            out.append((r.seq_len, r.seq_len))
+    for d in dreqs:
+        if d.flags & refresh_flag:
+            out.append((d.seq_len, d.seq_len))
         elif mode == "dual":
-            out.append((r.block_len, r.seq_len))
+            out.append((d.block_len, d.seq_len))
         else:
-            out.append((r.seq_len - s, r.seq_len))
+            out.append((d.seq_len - d.block_start, d.seq_len))
     return out
 
 
@@ -465,13 +465,15 @@ def main():
                 eng.release(slots[b])
                 slots[b] = make(b)
                 eng.admit(slots[b], cfg.mask_id)
-        rows = step_rows(slots, w.cache_mode)
-        m = sum(r.masked_in_block for r in slots)
-        refresh = sum(1 for r in slots
-                      if w.cache_mode == "none" or r.refreshed_block != r.block_start)
         ts = time.perf_counter()
-        eng.enqueue_step(slots)
-        if account:                       # host bookkeeping while the GPU runs the step
+        dreqs = eng.enqueue_step(slots)
+        # host bookkeeping while the GPU runs the step (from the descriptors
+        # the step was launched with; a step changes no block or mask count
+        # on the host before its read-back)
+        rows = launched_rows(dreqs, w.cache_mode, dlm.DLM_REQ_REFRESH)
+        m = sum(r.masked_in_block for r in slots)
+        refresh = sum(1 for d in dreqs if d.flags & dlm.DLM_REQ_REFRESH)
+        if account:
             account_step(rows, m, refresh)
         if prof_acc is not None:
             for k, (f, bb) in class_work(shape, rows, m).items():

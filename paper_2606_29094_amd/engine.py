@@ -103,13 +103,11 @@ class Request:
     steps: int = 0
     unmasked: int = 0
 
-    @property
-    def prompt_len(self):
-        return len(self.prompt)
-
-    @property
-    def seq_len(self):
-        return len(self.prompt) + self.gen_len
+    def __post_init__(self):
+        # fixed for the request's life and read for every request of every
+        # step: plain attributes keep the host's per-step work short
+        self.prompt_len = len(self.prompt)
+        self.seq_len = self.prompt_len + self.gen_len
 
     @property
     def block_start(self):
@@ -221,12 +219,17 @@ class Engine:
 
     # ---- one step
     def dlm_reqs(self, reqs: List[Request], force_refresh: bool = False):
+        # runs between a step's read-back and the next step's launch, while
+        # the GPU waits: one pass, no property calls
+        all_refresh = force_refresh or self.mode_id == dlm.DLM_CACHE_NONE
+        flag = dlm.DLM_REQ_REFRESH
+        make = dlm.DlmReq
         out = []
         for r in reqs:
-            s = r.block_start
-            refresh = force_refresh or self.mode_id == dlm.DLM_CACHE_NONE or r.refreshed_block != s
-            out.append(dlm.DlmReq(r.slot, r.seq_len, r.prompt_len, s, r.block_len, r.tok_offset,
-                                  dlm.DLM_REQ_REFRESH if refresh else 0))
+            s = r.prompt_len + r.k * r.block
+            n = r.seq_len - s
+            out.append(make(r.slot, r.seq_len, r.prompt_len, s, r.block if r.block < n else n,
+                            r.tok_offset, flag if all_refresh or r.refreshed_block != s else 0))
         return out
 
     def enqueue_step(self, reqs: List[Request], stream=None, force_refresh: bool = False):
